@@ -1,0 +1,144 @@
+/*
+ * som.h -- C ABI of the best-matching-unit (BMU) search for sparse binary
+ * documents against a feature-major codebook, on one AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The search (paper, Section 3 "Background: the design being tuned"): for
+ * each document x, a binary vector with feature set S, return the neuron j
+ * closest to x in squared Euclidean distance,
+ *
+ *     d_j = ||x - w_j||^2 = |S| + ||w_j||^2 - 2 * sum_{f in S} W[f][j],
+ *
+ * with the codebook stored feature-major (each feature's weights contiguous
+ * across neurons, W[f * ldw + j]), which turns the search into a tiled
+ * sparse-dense product whose argmin is fused into the product (same
+ * section).  Ties go to the lowest neuron index.
+ *
+ * Conventions for every entry point:
+ *  - Pointers are DEVICE pointers owned by the caller unless stated.  The
+ *    library allocates nothing and keeps no pointer after it returns.
+ *  - Work is enqueued asynchronously on `stream` (0 = the legacy default
+ *    stream); buffers must stay alive until that work completes.
+ *  - Argument errors are detected on the host before any HIP call and
+ *    return SOM_ERR_INVALID_ARG (or SOM_ERR_WORKSPACE); nothing is enqueued
+ *    then.  A failed launch returns SOM_ERR_HIP.  som_last_error() holds a
+ *    message for the last failure on the calling thread.
+ *  - No entry point throws, aborts or exits.
+ *  - Documents are CSR: indptr int32[B+1] with indptr[0] == 0 and
+ *    indptr[B] == nnz, indices int32[nnz] strictly ascending within each row
+ *    (a binary vector lists each feature once) and in [0, F).  Empty rows
+ *    are allowed.  Malformed CSR is undefined behaviour unless
+ *    opts->validate is set, in which case it is detected on the device and
+ *    reported as SOM_ERR_INVALID_CSR before any search work runs.
+ *  - Non-finite weights are undefined behaviour.
+ */
+#ifndef SOM_H
+#define SOM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum som_status {
+  SOM_OK = 0,
+  SOM_ERR_INVALID_ARG = 1, /* bad size, null pointer, misaligned or bad layout */
+  SOM_ERR_INVALID_CSR = 2, /* only with opts->validate: unsorted, duplicate or out-of-range ids */
+  SOM_ERR_WORKSPACE = 3,   /* ws too small (see som_*_workspace_bytes) */
+  SOM_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+} som_status;
+
+/* Tuning knobs of som_bmu_search.  A zero-initialised struct (or NULL)
+ * selects the defaults. */
+typedef struct som_bmu_opts {
+  int32_t tile_docs;    /* T, documents per tile (Section 4.1): 0 = auto, else 1, 2, 4, 8, 16 or 32 */
+  int32_t neuron_chunk; /* neurons per partial-argmin chunk (Section 4.2): 0 = auto, else a multiple of 2048 */
+  int32_t validate;     /* 1 = check the CSR batch on the device first (synchronises `stream`) */
+  int32_t reserved;     /* must be 0 */
+} som_bmu_opts;
+
+/* Version of this ABI (bumped on any incompatible change). */
+int32_t som_abi_version(void);
+
+/* Message describing the last failure on the calling thread; never NULL,
+ * "" when the last call succeeded.  Valid until the thread's next call. */
+const char* som_last_error(void);
+
+/* ||w_j||^2 for j < N (Section 3; the per-epoch "norms" pass of Table 4).
+ *   W      fp32 [F][ldw], feature-major, 16-byte aligned, ldw >= N, ldw % 4 == 0
+ *   norms  fp32 [N] output: each sum of squares is accumulated in fp64 in a
+ *          fixed order and rounded to fp32 once (deterministic).
+ * Errors: SOM_ERR_INVALID_ARG for F < 1, N < 1, bad ldw/alignment or NULL. */
+som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
+                              hipStream_t stream);
+
+/* Bytes of device workspace som_bmu_search needs for these sizes and
+ * options (0 if the arguments are invalid). */
+size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
+                               const som_bmu_opts* opts);
+
+/* BMU of each document of a CSR batch (Section 3; tiles of documents sweep
+ * the union of their features once, Section 4.1; the neuron axis is cut
+ * into chunks whose partial minima are merged, Section 4.2; the argmin is
+ * fused, never materialising the document x neuron score block).
+ *   W       fp32 [F][ldw] feature-major codebook (as for som_codebook_norms)
+ *   norms   fp32 [N] from som_codebook_norms of the same W
+ *   indptr  int32 [B+1], indices int32 [nnz]: the batch (see conventions)
+ *   perm    int32 [B] or NULL: tile order.  Position p of the tiled order
+ *           holds input document perm[p] (a permutation of 0..B-1, e.g. from
+ *           som_cluster_order); NULL = input order.  Results are always in
+ *           input order.
+ *   bmu     int32 [B] output: argmin_j d_j (lowest index on exact ties)
+ *   dist    fp32 [B] output: d_bmu, the squared distance |S| + ||w||^2 - 2 dot
+ *           evaluated in fp32 (dot summed in ascending feature order)
+ *   ws      device workspace of at least som_bmu_workspace_bytes(...) bytes,
+ *           256-byte aligned
+ * B == 0 is a valid no-op. */
+som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                          const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                          const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Tile plan (Section 4.1): for each tile of T consecutive documents of the
+ * tiled order (perm as in som_bmu_search; the last tile may be short) the
+ * sorted union of their features and, per union entry, a T-bit membership
+ * mask (bit s set iff the tile's s-th document contains the feature).
+ *   tile_docs   T in {1, 2, 4, 8, 16, 32}
+ *   tile_offset int32 [ntiles+1] output, ntiles = ceil(B / T): tile t's union
+ *               is stored at [tile_offset[t], tile_offset[t] + tile_count[t]);
+ *               tile_offset[t] is the number of nonzeros of tiles < t
+ *   tile_count  int32 [ntiles] output: |U_t|
+ *   union_feat  int32 [nnz] output (entries past each tile's count are unused)
+ *   union_mask  uint32 [nnz] output
+ *   ws          at least som_tile_plan_workspace_bytes(B, tile_docs) bytes
+ * This is the first stage of som_bmu_search, exported so that it can be
+ * checked on its own. */
+size_t som_tile_plan_workspace_bytes(int64_t B, int32_t tile_docs);
+som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                         int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,
+                         int32_t* tile_count, int32_t* union_feat, uint32_t* union_mask, void* ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+/* Tile-membership clustering (Section 4.2: documents that share descriptors
+ * are placed in the same tile, shrinking each tile's union).  The paper
+ * gives no algorithm; this is the label-free reading: df(f) = number of
+ * documents of the batch containing f; a document's signature is (s1, s2),
+ * its two features of highest df (ties to the lower id, F for a missing
+ * one); documents are ordered by (s1, s2, input position).
+ *   perm  int32 [B] output: perm[p] = input index of the document at position p
+ *   ws    at least som_cluster_workspace_bytes(B, F, nnz) bytes
+ * Deterministic; B == 0 is a no-op. */
+size_t som_cluster_workspace_bytes(int64_t B, int64_t F, int64_t nnz);
+som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                             int64_t nnz, int32_t* perm, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOM_H */

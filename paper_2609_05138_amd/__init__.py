@@ -1,0 +1,20 @@
+"""MI355X-native best-matching-unit (BMU) search for sparse binary documents.
+
+The compute lives in ``libsom.so`` (HIP kernels for gfx950 behind the C ABI
+of ``include/som.h``); ``paper_2609_05138_amd.som`` is the ctypes binding
+with the same function names.  Build with ``python -m
+paper_2609_05138_amd.build``.
+"""
+
+from .som import (  # noqa: F401
+    SomError,
+    load,
+    som_abi_version,
+    som_bmu_search,
+    som_bmu_workspace_bytes,
+    som_cluster_order,
+    som_cluster_workspace_bytes,
+    som_codebook_norms,
+    som_last_error,
+    som_tile_plan,
+)

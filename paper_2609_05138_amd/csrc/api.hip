@@ -1,0 +1,292 @@
+// C ABI of libsom (declared in include/som.h): host-side argument checks,
+// workspace carving and kernel sequencing.  No entry point allocates device
+// memory; every array comes from the caller.
+#include <string>
+
+#include "../../include/som.h"
+#include "common.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+som_status fail(som_status s, const std::string& msg) {
+  g_error = msg;
+  return s;
+}
+
+som_status ok() {
+  g_error.clear();
+  return SOM_OK;
+}
+
+som_status hip_fail(hipError_t e, const char* where) {
+  return fail(SOM_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+constexpr int64_t kI32Max = 2147483647;
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+som_status check_codebook(const float* W, int64_t F, int64_t N, int64_t ldw) {
+  if (!W) return fail(SOM_ERR_INVALID_ARG, "W is NULL");
+  if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
+  if (N < 1 || N > kI32Max) return fail(SOM_ERR_INVALID_ARG, "N must be in [1, 2^31)");
+  if (ldw < N) return fail(SOM_ERR_INVALID_ARG, "ldw must be >= N");
+  if (ldw % 4 != 0) return fail(SOM_ERR_INVALID_ARG, "ldw must be a multiple of 4");
+  if (!aligned(W, 16)) return fail(SOM_ERR_INVALID_ARG, "W must be 16-byte aligned");
+  return SOM_OK;
+}
+
+struct Plan {
+  int T = 8;
+  int K = 8;
+  int waves = 4;
+  int64_t ntiles = 0;
+  int64_t nchunks = 0;
+};
+
+som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
+  som_bmu_opts o{};
+  if (opts) o = *opts;
+  if (o.reserved != 0) return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
+  if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
+  int T = o.tile_docs ? o.tile_docs : 8;
+  if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
+    return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 1, 2, 4, 8, 16 or 32");
+  const int K = som::lanes_neurons(T);
+  const int64_t wave_n = 64 * K;
+  int waves;
+  if (o.neuron_chunk) {
+    if (o.neuron_chunk < 0 || o.neuron_chunk % wave_n != 0)
+      return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk must be a positive multiple of 64*K (512, or 256 for T=32)");
+    waves = static_cast<int>(o.neuron_chunk / wave_n);
+    if (waves != 1 && waves != 2 && waves != 4)
+      return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk must be 1, 2 or 4 waves of 64*K neurons");
+  } else {
+    const int64_t need = (N + wave_n - 1) / wave_n;
+    waves = need >= 4 ? 4 : (need >= 2 ? 2 : 1);
+  }
+  p->T = T;
+  p->K = K;
+  p->waves = waves;
+  p->ntiles = (B + T - 1) / T;
+  p->nchunks = (N + waves * wave_n - 1) / (waves * wave_n);
+  if (p->ntiles * p->nchunks > kI32Max)
+    return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: ceil(B/T) * chunks must be < 2^31");
+  return SOM_OK;
+}
+
+// Workspace layout of som_bmu_search (each region 256-byte aligned).
+struct SearchWs {
+  size_t tile_offset, tile_count, union_feat, union_mask, partial, flag, seen, total;
+};
+
+SearchWs search_ws(const Plan& p, int64_t B, int64_t nnz, bool validate) {
+  SearchWs w{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = som::align_up(o + (bytes ? bytes : 1), 256);
+    return at;
+  };
+  w.tile_offset = take(sizeof(int32_t) * (p.ntiles + 1));
+  w.tile_count = take(sizeof(int32_t) * p.ntiles);
+  w.union_feat = take(sizeof(int32_t) * nnz);
+  w.union_mask = take(sizeof(uint32_t) * nnz);
+  w.partial = take(sizeof(uint64_t) * p.nchunks * p.ntiles * p.T);
+  w.flag = take(sizeof(int32_t) * 4);
+  w.seen = validate ? take(sizeof(int32_t) * B) : 0;
+  w.total = o;
+  return w;
+}
+
+template <typename P>
+P* at(void* base, size_t off) {
+  return reinterpret_cast<P*>(static_cast<char*>(base) + off);
+}
+
+som_status check_batch(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz) {
+  if (B < 0 || B >= kI32Max) return fail(SOM_ERR_INVALID_ARG, "B must be in [0, 2^31 - 1)");
+  if (nnz < 0 || nnz > kI32Max) return fail(SOM_ERR_INVALID_ARG, "nnz must be in [0, 2^31)");
+  if (B > 0 && !indptr) return fail(SOM_ERR_INVALID_ARG, "indptr is NULL");
+  if (nnz > 0 && !indices) return fail(SOM_ERR_INVALID_ARG, "indices is NULL");
+  return SOM_OK;
+}
+
+som_status run_validate(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                        int64_t nnz, const int32_t* perm, int32_t* seen, int32_t* flag,
+                        hipStream_t stream) {
+  hipError_t e = som::launch_validate(indptr, indices, B, F, nnz, perm, seen, flag, stream);
+  if (e != hipSuccess) return hip_fail(e, "validate launch");
+  int32_t host_flag = 0;
+  e = hipMemcpyAsync(&host_flag, flag, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e != hipSuccess) return hip_fail(e, "validate read-back");
+  e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "validate synchronize");
+  if (host_flag) {
+    std::string why;
+    if (host_flag & 1) why += " indptr[0] != 0 or indptr[B] != nnz;";
+    if (host_flag & 2) why += " indptr not non-decreasing within [0, nnz];";
+    if (host_flag & 4) why += " feature ids out of [0, F) or not strictly ascending;";
+    if (host_flag & 8) why += " perm value out of [0, B);";
+    if (host_flag & 16) why += " perm repeats a document;";
+    return fail(SOM_ERR_INVALID_CSR, "invalid batch:" + why);
+  }
+  return SOM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t som_abi_version(void) { return 1; }
+
+const char* som_last_error(void) { return g_error.c_str(); }
+
+som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
+                              hipStream_t stream) {
+  som_status s = check_codebook(W, F, N, ldw);
+  if (s != SOM_OK) return s;
+  if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
+  hipError_t e = som::launch_norms(W, F, N, ldw, norms, stream);
+  if (e != hipSuccess) return hip_fail(e, "norms launch");
+  return ok();
+}
+
+size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz, const som_bmu_opts* opts) {
+  if (F < 1 || N < 1 || B < 0 || nnz < 0) return 0;
+  Plan p;
+  if (make_plan(N, B, opts, &p) != SOM_OK) return 0;
+  const bool validate = opts && opts->validate;
+  return search_ws(p, B, nnz, validate).total;
+}
+
+som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                          const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                          const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  som_status s = check_codebook(W, F, N, ldw);
+  if (s != SOM_OK) return s;
+  if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
+  s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (B > 0 && (!bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "bmu or dist is NULL");
+  Plan p;
+  s = make_plan(N, B, opts, &p);
+  if (s != SOM_OK) return s;
+  const bool validate = opts && opts->validate;
+  const SearchWs w = search_ws(p, B, nnz, validate);
+  if (B == 0) return ok();
+  if (!ws) return fail(SOM_ERR_WORKSPACE, "ws is NULL");
+  if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
+  if (ws_bytes < w.total)
+    return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(w.total) + " bytes");
+
+  if (validate) {
+    s = run_validate(indptr, indices, B, F, nnz, perm, at<int32_t>(ws, w.seen), at<int32_t>(ws, w.flag), stream);
+    if (s != SOM_OK) return s;
+  }
+  som::SearchArgs a{};
+  a.W = W;
+  a.F = F;
+  a.N = N;
+  a.ldw = ldw;
+  a.norms = norms;
+  a.indptr = indptr;
+  a.perm = perm;
+  a.B = B;
+  a.T = p.T;
+  a.waves = p.waves;
+  a.ntiles = p.ntiles;
+  a.nchunks = p.nchunks;
+  a.tile_offset = at<int32_t>(ws, w.tile_offset);
+  a.tile_count = at<int32_t>(ws, w.tile_count);
+  a.union_feat = at<int32_t>(ws, w.union_feat);
+  a.union_mask = at<uint32_t>(ws, w.union_mask);
+  a.partial = at<uint64_t>(ws, w.partial);
+  a.bmu = bmu;
+  a.dist = dist;
+  hipError_t e = som::launch_tile_plan(indptr, indices, B, F, perm, p.T, at<int32_t>(ws, w.tile_offset),
+                                       at<int32_t>(ws, w.tile_count), at<int32_t>(ws, w.union_feat),
+                                       at<uint32_t>(ws, w.union_mask), stream);
+  if (e != hipSuccess) return hip_fail(e, "tile plan launch");
+  e = som::launch_search(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "search launch");
+  e = som::launch_merge(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "merge launch");
+  return ok();
+}
+
+size_t som_tile_plan_workspace_bytes(int64_t B, int32_t tile_docs) {
+  (void)B;
+  (void)tile_docs;
+  return 0;
+}
+
+som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                         int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,
+                         int32_t* tile_count, int32_t* union_feat, uint32_t* union_mask, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  som_status s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
+  const int T = tile_docs;
+  if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
+    return fail(SOM_ERR_INVALID_ARG, "tile_docs must be 1, 2, 4, 8, 16 or 32");
+  if (B == 0) return ok();
+  if (!tile_offset || !tile_count || (nnz > 0 && (!union_feat || !union_mask)))
+    return fail(SOM_ERR_INVALID_ARG, "an output array is NULL");
+  hipError_t e = som::launch_tile_plan(indptr, indices, B, F, perm, T, tile_offset, tile_count,
+                                       union_feat, union_mask, stream);
+  if (e != hipSuccess) return hip_fail(e, "tile plan launch");
+  return ok();
+}
+
+size_t som_cluster_workspace_bytes(int64_t B, int64_t F, int64_t nnz) {
+  if (B < 0 || F < 1 || nnz < 0 || B >= kI32Max) return 0;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { o = som::align_up(o + (bytes ? bytes : 1), 256); };
+  take(sizeof(int32_t) * F);        // df
+  take(sizeof(uint64_t) * B);       // keys
+  take(sizeof(uint64_t) * B);       // sorted keys
+  take(sizeof(int32_t) * B);        // iota
+  take(som::cluster_sort_temp_bytes(B, F));
+  return o;
+}
+
+som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                             int64_t nnz, int32_t* perm, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  som_status s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
+  if (B == 0) return ok();
+  if (!perm) return fail(SOM_ERR_INVALID_ARG, "perm is NULL");
+  if (!ws) return fail(SOM_ERR_WORKSPACE, "ws is NULL");
+  if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
+  const size_t need = som_cluster_workspace_bytes(B, F, nnz);
+  if (ws_bytes < need)
+    return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t a = o;
+    o = som::align_up(o + (bytes ? bytes : 1), 256);
+    return a;
+  };
+  const size_t o_df = take(sizeof(int32_t) * F);
+  const size_t o_keys = take(sizeof(uint64_t) * B);
+  const size_t o_sorted = take(sizeof(uint64_t) * B);
+  const size_t o_iota = take(sizeof(int32_t) * B);
+  const size_t tb = som::cluster_sort_temp_bytes(B, F);
+  const size_t o_tmp = take(tb);
+  hipError_t e = som::launch_cluster(indptr, indices, B, F, nnz, perm, at<int32_t>(ws, o_df),
+                                     at<uint64_t>(ws, o_keys), at<uint64_t>(ws, o_sorted),
+                                     at<int32_t>(ws, o_iota), at<void>(ws, o_tmp), tb, stream);
+  if (e != hipSuccess) return hip_fail(e, "cluster launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,84 @@
+// Internal declarations shared by the HIP translation units of libsom.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace som {
+
+// Packed argmin key: the high 32 bits are the distance mapped to an unsigned
+// integer whose order matches the float order, the low 32 bits the neuron
+// index.  The unsigned 64-bit minimum of two keys is then the smaller
+// distance, and on equal distances the lower index -- associative and
+// commutative, so the reduction order never changes the answer.
+__device__ __forceinline__ uint32_t ordered_bits(float d) {
+  uint32_t u = __float_as_uint(d);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float from_ordered_bits(uint32_t u) {
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
+}
+
+__device__ __forceinline__ uint64_t pack_key(float d, uint32_t j) {
+  return (static_cast<uint64_t>(ordered_bits(d)) << 32) | j;
+}
+
+constexpr uint64_t kNoKey = ~0ull;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// Launchers (each enqueues on `stream` and returns the launch status).
+// ---------------------------------------------------------------------------
+
+hipError_t launch_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
+                        hipStream_t stream);
+
+// CSR (and optional permutation) checks; sets *flag (device int) nonzero on failure.
+hipError_t launch_validate(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                           int64_t nnz, const int32_t* perm, int32_t* seen, int32_t* flag,
+                           hipStream_t stream);
+
+// Tile plan: tile_offset[ntiles+1] (exclusive scan of per-tile nonzeros),
+// tile_count[ntiles], union_feat / union_mask (see som_tile_plan).
+hipError_t launch_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                            const int32_t* perm, int T, int32_t* tile_offset, int32_t* tile_count,
+                            int32_t* union_feat, uint32_t* union_mask, hipStream_t stream);
+
+struct SearchArgs {
+  const float* W;
+  int64_t F, N, ldw;
+  const float* norms;
+  const int32_t* indptr;
+  const int32_t* perm;
+  int64_t B;
+  int T;            // documents per tile
+  int waves;        // waves per workgroup (each covers 64 * K neurons)
+  int64_t ntiles;
+  int64_t nchunks;  // neuron chunks = ceil(N / (waves * 64 * K))
+  const int32_t* tile_offset;
+  const int32_t* tile_count;
+  const int32_t* union_feat;
+  const uint32_t* union_mask;
+  uint64_t* partial;  // [nchunks][ntiles * T]
+  int32_t* bmu;
+  float* dist;
+};
+
+// Neurons per lane for a tile size (VGPR budget: T * K accumulators).
+inline int lanes_neurons(int T) { return T >= 32 ? 4 : 8; }
+
+hipError_t launch_search(const SearchArgs& a, hipStream_t stream);
+hipError_t launch_merge(const SearchArgs& a, hipStream_t stream);
+
+// Clustering.
+size_t cluster_sort_temp_bytes(int64_t B, int64_t F);
+hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                          int64_t nnz, int32_t* perm, int32_t* df, uint64_t* keys,
+                          uint64_t* keys_sorted, int32_t* iota, void* sort_temp,
+                          size_t sort_temp_bytes, hipStream_t stream);
+
+}  // namespace som

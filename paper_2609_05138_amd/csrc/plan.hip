@@ -1,0 +1,215 @@
+// Tile plan (paper, Section 4.1): a tile of T documents forms the sorted
+// union of the distinct features its documents contain, so that each union
+// feature's codebook row is swept once for the whole tile.  Per union entry
+// the plan also records a T-bit membership mask (bit s: the tile's s-th
+// document contains the feature), which the search uses to add the row only
+// into the accumulators of the documents that hold it.
+//
+// Layout produced (all int32 unless noted):
+//   tile_offset[t]  = number of nonzeros in tiles < t (exclusive scan); the
+//                     union of tile t is stored from there, and since
+//                     |U_t| <= nnz(t) it never overlaps tile t + 1
+//   tile_count[t]   = |U_t|
+//   union_feat[.]   = ascending feature ids, union_mask[.] (uint32) = masks
+//
+// Construction: one workgroup per tile marks a bitmap of T-bit masks indexed
+// by feature (a window of up to 32768 features in LDS), then compacts the
+// nonzero entries in ascending order with a workgroup prefix sum.  Integer
+// work, bit-exact by construction.
+#include "common.h"
+
+namespace som {
+namespace {
+
+constexpr int kPlanThreads = 256;
+constexpr int kPlanWindow = 32768;  // features per LDS window (128 KB of masks)
+
+__device__ __forceinline__ int64_t tile_doc(const int32_t* perm, int64_t p) {
+  return perm ? static_cast<int64_t>(perm[p]) : p;
+}
+
+__global__ void __launch_bounds__(256)
+k_tile_nnz(const int32_t* __restrict__ indptr, const int32_t* __restrict__ perm, int64_t B, int T,
+           int64_t ntiles, int32_t* __restrict__ tile_nnz) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= ntiles) return;
+  int32_t s = 0;
+  for (int k = 0; k < T; ++k) {
+    const int64_t p = t * T + k;
+    if (p < B) {
+      const int64_t d = tile_doc(perm, p);
+      s += indptr[d + 1] - indptr[d];
+    }
+  }
+  tile_nnz[t] = s;
+}
+
+// Exclusive scan of n values in place into out[0..n] (out[n] = total), one
+// workgroup of 1024 threads; each thread scans a contiguous run.
+__global__ void __launch_bounds__(1024)
+k_scan(const int32_t* __restrict__ in, int64_t n, int32_t* __restrict__ out) {
+  __shared__ int32_t sums[1024];
+  const int tid = threadIdx.x;
+  const int64_t per = (n + 1023) / 1024;
+  const int64_t a = tid * per;
+  const int64_t b = a + per < n ? a + per : n;
+  int32_t s = 0;
+  for (int64_t i = a; i < b; ++i) s += in[i];
+  sums[tid] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int32_t v = tid >= off ? sums[tid - off] : 0;
+    __syncthreads();
+    sums[tid] += v;
+    __syncthreads();
+  }
+  int32_t run = tid ? sums[tid - 1] : 0;
+  for (int64_t i = a; i < b; ++i) {
+    const int32_t v = in[i];
+    out[i] = run;
+    run += v;
+  }
+  if (tid == 1023) out[n] = sums[1023];
+}
+
+// Workgroup exclusive prefix sum of one value per thread (256 threads).
+__device__ int32_t block_exclusive_scan(int32_t v, int32_t* tmp, int32_t* total) {
+  const int tid = threadIdx.x;
+  tmp[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < kPlanThreads; off <<= 1) {
+    const int32_t x = tid >= off ? tmp[tid - off] : 0;
+    __syncthreads();
+    tmp[tid] += x;
+    __syncthreads();
+  }
+  const int32_t incl = tmp[tid];
+  *total = tmp[kPlanThreads - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ void __launch_bounds__(kPlanThreads)
+k_plan(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
+       const int32_t* __restrict__ perm, int64_t B, int64_t F, int T, int window,
+       const int32_t* __restrict__ tile_offset, int32_t* __restrict__ tile_count,
+       int32_t* __restrict__ union_feat, uint32_t* __restrict__ union_mask) {
+  extern __shared__ uint32_t bits[];  // [window]
+  __shared__ int32_t tmp[kPlanThreads];
+  const int tid = threadIdx.x;
+  const int64_t t = blockIdx.x;
+  const int64_t out0 = tile_offset[t];
+  int32_t written = 0;
+  for (int64_t w0 = 0; w0 < F; w0 += window) {
+    const int wlen = static_cast<int>(F - w0 < window ? F - w0 : window);
+    for (int i = tid; i < wlen; i += kPlanThreads) bits[i] = 0u;
+    __syncthreads();
+    for (int k = 0; k < T; ++k) {
+      const int64_t p = t * T + k;
+      if (p >= B) break;
+      const int64_t d = tile_doc(perm, p);
+      const int32_t a = indptr[d], b = indptr[d + 1];
+      for (int32_t i = a + tid; i < b; i += kPlanThreads) {
+        const int64_t f = indices[i];
+        if (f >= w0 && f < w0 + wlen) atomicOr(&bits[f - w0], 1u << k);
+      }
+    }
+    __syncthreads();
+    // each thread compacts a contiguous run of the window, in order
+    const int per = (wlen + kPlanThreads - 1) / kPlanThreads;
+    const int a = tid * per;
+    const int b = a + per < wlen ? a + per : wlen;
+    int32_t cnt = 0;
+    for (int i = a; i < b; ++i) cnt += bits[i] != 0u;
+    int32_t total;
+    int32_t pos = block_exclusive_scan(cnt, tmp, &total);
+    for (int i = a; i < b; ++i) {
+      const uint32_t m = bits[i];
+      if (m) {
+        const int64_t o = out0 + written + pos;
+        union_feat[o] = static_cast<int32_t>(w0 + i);
+        union_mask[o] = m;
+        ++pos;
+      }
+    }
+    written += total;
+    __syncthreads();
+  }
+  if (tid == 0) tile_count[t] = written;
+}
+
+// CSR checks: rows non-decreasing in indptr, ids in [0, F) and strictly
+// ascending within a row; optional permutation must hit every index once.
+__global__ void __launch_bounds__(256)
+k_validate(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, int64_t B,
+           int64_t F, int64_t nnz, const int32_t* __restrict__ perm, int32_t* __restrict__ seen,
+           int32_t* __restrict__ flag) {
+  const int64_t d = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (d == 0 && (indptr[0] != 0 || indptr[B] != nnz)) atomicOr(flag, 1);
+  if (d >= B) return;
+  const int32_t a = indptr[d], b = indptr[d + 1];
+  if (a > b || a < 0 || b > nnz) {
+    atomicOr(flag, 2);
+    return;
+  }
+  int64_t prev = -1;
+  for (int32_t i = a; i < b; ++i) {
+    const int64_t f = indices[i];
+    if (f < 0 || f >= F || f <= prev) {
+      atomicOr(flag, 4);
+      break;
+    }
+    prev = f;
+  }
+  if (perm) {
+    const int64_t q = perm[d];
+    if (q < 0 || q >= B) {
+      atomicOr(flag, 8);
+    } else if (atomicAdd(&seen[q], 1) != 0) {
+      atomicOr(flag, 16);
+    }
+  }
+}
+
+__global__ void k_fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+}  // namespace
+
+hipError_t launch_validate(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                           int64_t nnz, const int32_t* perm, int32_t* seen, int32_t* flag,
+                           hipStream_t stream) {
+  hipLaunchKernelGGL(k_fill_i32, dim3(1), dim3(64), 0, stream, flag, int64_t(1), 0);
+  if (perm) {
+    hipLaunchKernelGGL(k_fill_i32, dim3(static_cast<uint32_t>((B + 255) / 256)), dim3(256), 0,
+                       stream, seen, B, 0);
+  }
+  const int64_t groups = (B + 255) / 256;
+  hipLaunchKernelGGL(k_validate, dim3(static_cast<uint32_t>(groups > 0 ? groups : 1)), dim3(256),
+                     0, stream, indptr, indices, B, F, nnz, perm, seen, flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                            const int32_t* perm, int T, int32_t* tile_offset, int32_t* tile_count,
+                            int32_t* union_feat, uint32_t* union_mask, hipStream_t stream) {
+  const int64_t ntiles = (B + T - 1) / T;
+  // per-tile nonzeros are staged in tile_count, then scanned into tile_offset
+  hipLaunchKernelGGL(k_tile_nnz, dim3(static_cast<uint32_t>((ntiles + 255) / 256)), dim3(256), 0,
+                     stream, indptr, perm, B, T, ntiles, tile_count);
+  hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, tile_count, ntiles, tile_offset);
+  const int window = static_cast<int>(F < kPlanWindow ? F : kPlanWindow);
+  const size_t lds = sizeof(uint32_t) * static_cast<size_t>(window);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_plan),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     static_cast<int>(lds));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_plan, dim3(static_cast<uint32_t>(ntiles)), dim3(kPlanThreads), lds, stream,
+                     indptr, indices, perm, B, F, T, window, tile_offset, tile_count, union_feat,
+                     union_mask);
+  return hipGetLastError();
+}
+
+}  // namespace som

@@ -1,0 +1,243 @@
+"""Thin ctypes binding of libsom (include/som.h) for torch device tensors.
+
+Argument marshalling only: every step of the search runs in the HIP
+library.  There is no CPU path: if the library is not built, or a tensor is
+not on a ROCm device, calls raise.  Function names match the C entry points.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch  # imported before the library so both share one HIP runtime
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsom.so")
+
+SOM_OK = 0
+SOM_ERR_INVALID_ARG = 1
+SOM_ERR_INVALID_CSR = 2
+SOM_ERR_WORKSPACE = 3
+SOM_ERR_HIP = 4
+
+EXPORTS = (
+    "som_abi_version",
+    "som_last_error",
+    "som_codebook_norms",
+    "som_bmu_workspace_bytes",
+    "som_bmu_search",
+    "som_tile_plan_workspace_bytes",
+    "som_tile_plan",
+    "som_cluster_workspace_bytes",
+    "som_cluster_order",
+)
+
+
+class SomError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"libsom status {status}: {msg}")
+        self.status = status
+
+
+class som_bmu_opts(ctypes.Structure):
+    _fields_ = [
+        ("tile_docs", ctypes.c_int32),
+        ("neuron_chunk", ctypes.c_int32),
+        ("validate", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+_i64 = ctypes.c_int64
+_i32 = ctypes.c_int32
+_vp = ctypes.c_void_p
+_sz = ctypes.c_size_t
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libsom.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(
+            f"{path} is missing: build it with `python -m paper_2609_05138_amd.build` "
+            "(there is no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    lib.som_abi_version.restype = _i32
+    lib.som_abi_version.argtypes = []
+    lib.som_last_error.restype = ctypes.c_char_p
+    lib.som_last_error.argtypes = []
+    lib.som_codebook_norms.restype = _i32
+    lib.som_codebook_norms.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp]
+    lib.som_bmu_workspace_bytes.restype = _sz
+    lib.som_bmu_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, ctypes.POINTER(som_bmu_opts)]
+    lib.som_bmu_search.restype = _i32
+    lib.som_bmu_search.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp,
+                                   ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
+    lib.som_tile_plan_workspace_bytes.restype = _sz
+    lib.som_tile_plan_workspace_bytes.argtypes = [_i64, _i32]
+    lib.som_tile_plan.restype = _i32
+    lib.som_tile_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.som_cluster_workspace_bytes.restype = _sz
+    lib.som_cluster_workspace_bytes.argtypes = [_i64, _i64, _i64]
+    lib.som_cluster_order.restype = _i32
+    lib.som_cluster_order.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _sz, _vp]
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != SOM_OK:
+        raise SomError(status, load().som_last_error().decode(errors="replace"))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, dtype, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a ROCm device (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _opts(tile_docs=0, neuron_chunk=0, validate=False) -> som_bmu_opts:
+    return som_bmu_opts(int(tile_docs), int(neuron_chunk), int(bool(validate)), 0)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns 256-byte (or better) aligned blocks
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def som_abi_version() -> int:
+    return int(load().som_abi_version())
+
+
+def som_last_error() -> str:
+    return load().som_last_error().decode(errors="replace")
+
+
+def som_codebook_norms(W: torch.Tensor, N: Optional[int] = None, norms: Optional[torch.Tensor] = None,
+                       stream=None) -> torch.Tensor:
+    """||w_j||^2 for j < N of the feature-major codebook W [F, ldw] (fp32)."""
+    lib = load()
+    _dev(W, torch.float32, "W")
+    F, ldw = W.shape
+    n = ldw if N is None else int(N)
+    if norms is None:
+        norms = torch.empty(n, dtype=torch.float32, device=W.device)
+    _dev(norms, torch.float32, "norms")
+    if norms.numel() < n:
+        raise ValueError("norms is too small")
+    _check(lib.som_codebook_norms(_ptr(W), F, n, ldw, _ptr(norms), _stream(stream)))
+    return norms
+
+
+def som_bmu_workspace_bytes(F: int, N: int, B: int, nnz: int, tile_docs=0, neuron_chunk=0,
+                            validate=False) -> int:
+    o = _opts(tile_docs, neuron_chunk, validate)
+    return int(load().som_bmu_workspace_bytes(F, N, B, nnz, ctypes.byref(o)))
+
+
+def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, indices: torch.Tensor,
+                   N: Optional[int] = None, perm: Optional[torch.Tensor] = None, tile_docs: int = 0,
+                   neuron_chunk: int = 0, validate: bool = False, bmu: Optional[torch.Tensor] = None,
+                   dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """BMU index (int32) and squared distance (fp32) of every CSR document."""
+    lib = load()
+    _dev(W, torch.float32, "W")
+    _dev(norms, torch.float32, "norms")
+    _dev(indptr, torch.int32, "indptr")
+    _dev(indices, torch.int32, "indices")
+    F, ldw = W.shape
+    n = ldw if N is None else int(N)
+    B = indptr.numel() - 1
+    nnz = indices.numel()
+    if perm is not None:
+        _dev(perm, torch.int32, "perm")
+        if perm.numel() != B:
+            raise ValueError("perm must have B entries")
+    if bmu is None:
+        bmu = torch.empty(B, dtype=torch.int32, device=W.device)
+    if dist is None:
+        dist = torch.empty(B, dtype=torch.float32, device=W.device)
+    _dev(bmu, torch.int32, "bmu")
+    _dev(dist, torch.float32, "dist")
+    if bmu.numel() < B or dist.numel() < B:
+        raise ValueError("bmu / dist are too small")
+    o = _opts(tile_docs, neuron_chunk, validate)
+    need = int(lib.som_bmu_workspace_bytes(F, n, B, nnz, ctypes.byref(o)))
+    if ws is None:
+        ws = _workspace(need, W.device)
+    _dev(ws, torch.uint8, "ws")
+    _check(lib.som_bmu_search(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), _ptr(indices), B, nnz,
+                              _ptr(perm), _ptr(bmu), _ptr(dist), ctypes.byref(o), _ptr(ws),
+                              ws.numel(), _stream(stream)))
+    return bmu, dist
+
+
+def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs: int,
+                  perm: Optional[torch.Tensor] = None, stream=None):
+    """(tile_offset, tile_count, union_feat, union_mask) of the tiled order."""
+    lib = load()
+    _dev(indptr, torch.int32, "indptr")
+    _dev(indices, torch.int32, "indices")
+    B = indptr.numel() - 1
+    nnz = indices.numel()
+    T = int(tile_docs)
+    ntiles = (B + T - 1) // T if T > 0 else 0
+    dev = indptr.device
+    if perm is not None:
+        _dev(perm, torch.int32, "perm")
+    tile_offset = torch.empty(ntiles + 1, dtype=torch.int32, device=dev)
+    tile_count = torch.empty(max(ntiles, 1), dtype=torch.int32, device=dev)
+    union_feat = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    union_mask = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    ws_bytes = int(lib.som_tile_plan_workspace_bytes(B, T))
+    ws = _workspace(ws_bytes, dev)
+    _check(lib.som_tile_plan(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), T, _ptr(tile_offset),
+                             _ptr(tile_count), _ptr(union_feat), _ptr(union_mask), _ptr(ws), ws.numel(),
+                             _stream(stream)))
+    return tile_offset, tile_count[:ntiles], union_feat, union_mask
+
+
+def som_cluster_workspace_bytes(B: int, F: int, nnz: int) -> int:
+    return int(load().som_cluster_workspace_bytes(B, F, nnz))
+
+
+def som_cluster_order(indptr: torch.Tensor, indices: torch.Tensor, F: int,
+                      perm: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """Tile order grouping documents by their two highest-df features."""
+    lib = load()
+    _dev(indptr, torch.int32, "indptr")
+    _dev(indices, torch.int32, "indices")
+    B = indptr.numel() - 1
+    nnz = indices.numel()
+    if perm is None:
+        perm = torch.empty(max(B, 1), dtype=torch.int32, device=indptr.device)
+    _dev(perm, torch.int32, "perm")
+    if ws is None:
+        ws = _workspace(lib.som_cluster_workspace_bytes(B, F, nnz), indptr.device)
+    _dev(ws, torch.uint8, "ws")
+    _check(lib.som_cluster_order(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), _ptr(ws), ws.numel(),
+                                 _stream(stream)))
+    return perm[:B]

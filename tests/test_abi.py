@@ -1,0 +1,138 @@
+"""C ABI checks that need no GPU: the library loads, exports every entry point
+the header declares, and rejects bad arguments on the host before any HIP
+call (so these run on a machine without a GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+
+som = pytest.importorskip("paper_2609_05138_amd.som")
+
+HEADER = os.path.join(ROOT, "include", "som.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(som_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(som.LIB_PATH):
+        pytest.fail("libsom.so is not built (run python -m paper_2609_05138_amd.build)")
+    return som.load()
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for must in ("som_codebook_norms", "som_bmu_search", "som_bmu_workspace_bytes",
+                 "som_tile_plan", "som_cluster_order", "som_last_error"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_declared()) == set(som.EXPORTS)
+
+
+def test_abi_version(lib):
+    assert som.som_abi_version() == 1
+
+
+def test_workspace_sizes_are_host_only(lib):
+    o = som.som_bmu_opts(0, 0, 0, 0)
+    a = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o))
+    assert a > 0 and a % 256 == 0
+    # partial keys [chunks][B] dominate: 128 chunks x 1M docs x 8 B
+    assert a >= 128 * (1 << 20) * 8
+    o8 = som.som_bmu_opts(16, 1024, 1, 0)
+    b = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o8))
+    assert b > a
+    assert lib.som_bmu_workspace_bytes(0, 10, 10, 10, None) == 0
+    assert lib.som_bmu_workspace_bytes(10, 10, -1, 10, None) == 0
+    bad = som.som_bmu_opts(3, 0, 0, 0)
+    assert lib.som_bmu_workspace_bytes(10, 10, 10, 10, ctypes.byref(bad)) == 0
+
+
+def _status(lib, fn, *args):
+    st = getattr(lib, fn)(*args)
+    return st, lib.som_last_error().decode()
+
+
+def test_norms_rejects_bad_arguments(lib):
+    null = None
+    fake = ctypes.c_void_p(0x1000)            # never dereferenced: rejected first
+    mis = ctypes.c_void_p(0x1004)
+    assert _status(lib, "som_codebook_norms", null, 4, 4, 4, fake, null)[0] == som.SOM_ERR_INVALID_ARG
+    assert _status(lib, "som_codebook_norms", fake, 0, 4, 4, fake, null)[0] == som.SOM_ERR_INVALID_ARG
+    assert _status(lib, "som_codebook_norms", fake, 4, 0, 4, fake, null)[0] == som.SOM_ERR_INVALID_ARG
+    st, msg = _status(lib, "som_codebook_norms", fake, 4, 8, 4, fake, null)
+    assert st == som.SOM_ERR_INVALID_ARG and "ldw" in msg
+    assert _status(lib, "som_codebook_norms", fake, 4, 5, 6, fake, null)[0] == som.SOM_ERR_INVALID_ARG
+    st, msg = _status(lib, "som_codebook_norms", mis, 4, 4, 4, fake, null)
+    assert st == som.SOM_ERR_INVALID_ARG and "aligned" in msg
+    assert _status(lib, "som_codebook_norms", fake, 4, 4, 4, null, null)[0] == som.SOM_ERR_INVALID_ARG
+
+
+def test_search_rejects_bad_arguments(lib):
+    null = None
+    fake = ctypes.c_void_p(0x1000)
+    ws_bad = ctypes.c_void_p(0x1010)
+    o = som.som_bmu_opts(0, 0, 0, 0)
+    args = dict(W=fake, F=8, N=8, ldw=8, norms=fake, indptr=fake, indices=fake, B=4, nnz=10,
+                perm=null, bmu=fake, dist=fake, opts=ctypes.byref(o), ws=fake, ws_bytes=1 << 30,
+                stream=null)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return _status(lib, "som_bmu_search", *a.values())
+
+    assert call(W=null)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(norms=null)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(indptr=null)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(indices=null)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(bmu=null)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(B=-1)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(nnz=-1)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(ldw=6)[0] == som.SOM_ERR_INVALID_ARG
+    st, msg = call(ws_bytes=16)
+    assert st == som.SOM_ERR_WORKSPACE and "need" in msg
+    assert call(ws=null)[0] == som.SOM_ERR_WORKSPACE
+    assert call(ws=ws_bad)[0] == som.SOM_ERR_INVALID_ARG
+    for bad in (som.som_bmu_opts(3, 0, 0, 0), som.som_bmu_opts(0, 300, 0, 0),
+                som.som_bmu_opts(0, 0, 2, 0), som.som_bmu_opts(0, 0, 0, 1),
+                som.som_bmu_opts(8, 512 * 8, 0, 0)):
+        st, msg = call(opts=ctypes.byref(bad))
+        assert st == som.SOM_ERR_INVALID_ARG, msg
+    # an empty batch is a valid no-op that touches nothing
+    assert call(B=0, nnz=0, indices=null, bmu=null, dist=null, ws=null, ws_bytes=0)[0] == som.SOM_OK
+    assert lib.som_last_error().decode() == ""
+
+
+def test_plan_and_cluster_reject_bad_arguments(lib):
+    null = None
+    fake = ctypes.c_void_p(0x1000)
+    st, msg = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 3, fake, fake, fake, fake, null, 0, null)
+    assert st == som.SOM_ERR_INVALID_ARG and "tile_docs" in msg
+    st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 0, 10, null, 4, fake, fake, fake, fake, null, 0, null)
+    assert st == som.SOM_ERR_INVALID_ARG
+    st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 4, null, fake, fake, fake, null, 0, null)
+    assert st == som.SOM_ERR_INVALID_ARG
+    st, _ = _status(lib, "som_cluster_order", fake, fake, 4, 8, 10, null, fake, 1 << 20, null)
+    assert st == som.SOM_ERR_INVALID_ARG
+    st, _ = _status(lib, "som_cluster_order", fake, fake, 4, 8, 10, fake, null, 1 << 20, null)
+    assert st == som.SOM_ERR_WORKSPACE
+    assert _status(lib, "som_cluster_order", null, null, 0, 8, 0, null, null, 0, null)[0] == som.SOM_OK
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    W = torch.zeros(4, 4)
+    with pytest.raises(ValueError):
+        som.som_codebook_norms(W)

@@ -1,0 +1,316 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle.
+
+Bit-exact where the arithmetic is exact (integer plan and clustering work,
+dyadic codebooks whose every fp32 sum is exact, the hand-worked examples);
+elsewhere the acceptance rule of the search: the device index equals the
+oracle's BMU unless it lies in the oracle's 1e-5 relative near-tie band, and
+the device distance is within 1e-5 relative of the oracle's distance for
+that index.
+"""
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import GOLDEN
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2609_05138_amd as som
+else:  # collected on CPU-only machines, never run there
+    som = None
+
+DEV = "cuda:0"
+REL = 1e-5
+
+
+def _csr(docs):
+    indptr = np.zeros(len(docs) + 1, np.int64)
+    indptr[1:] = np.cumsum([len(d) for d in docs])
+    indices = np.array([f for d in docs for f in d], dtype=np.int64)
+    return indptr, indices
+
+
+def _dev_i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(DEV)
+
+
+def _dev_W(W, ldw=None):
+    F, N = W.shape
+    ld = ((N + 3) // 4 * 4) if ldw is None else ldw
+    Wp = np.zeros((F, ld), np.float32)
+    Wp[:, :N] = W
+    return torch.from_numpy(Wp).to(DEV), ld
+
+
+def _search(W, indptr, indices, N=None, ldw=None, perm=None, **kw):
+    Wd, ld = _dev_W(W, ldw)
+    n = W.shape[1] if N is None else N
+    norms = som.som_codebook_norms(Wd, N=n)
+    p = None if perm is None else _dev_i32(perm)
+    bmu, dist = som.som_bmu_search(Wd, norms, _dev_i32(indptr), _dev_i32(indices), N=n, perm=p, **kw)
+    torch.cuda.synchronize()
+    return bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64), norms.cpu().numpy()
+
+
+def _random_docs(rng, B, F, mean, empty_every=0, big_every=0, big=0):
+    docs = []
+    for i in range(B):
+        k = min(F, int(rng.poisson(mean)))
+        if empty_every and i % empty_every == 0:
+            k = 0
+        if big_every and i % big_every == 1:
+            k = min(F, big)
+        docs.append(sorted(rng.choice(F, k, replace=False).tolist()))
+    return docs
+
+
+TILES = [1, 2, 4, 8, 16, 32]
+
+
+# ----------------------------------------------------------------------------
+# norms
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("F,N,pad", [(1, 1, 3), (7, 5, 0), (300, 1025, 4), (2048, 1024, 0), (129, 4099, 61)])
+def test_norms_match_oracle(F, N, pad):
+    rng = np.random.default_rng(F * 7 + N)
+    W = rng.random((F, N), dtype=np.float32)
+    ldw = (N + 3) // 4 * 4 + (pad // 4) * 4
+    Wd, _ = _dev_W(W, ldw)
+    got = som.som_codebook_norms(Wd, N=N).cpu().numpy()
+    want = oracle.codebook_norms(W.astype(np.float64))
+    # fp64 accumulation rounded once: equal to the correctly rounded value
+    # except within fp64 rounding of a half-way point (at most 1 ulp)
+    want32 = want.astype(np.float32)
+    ulps = np.abs(got.view(np.int32).astype(np.int64) - want32.view(np.int32).astype(np.int64))
+    assert ulps.max() <= 1
+    assert np.count_nonzero(ulps) <= max(1, N // 1000)
+
+
+def test_norms_dyadic_bit_exact():
+    rng = np.random.default_rng(1)
+    W = rng.integers(0, 4, (500, 777)).astype(np.float32) / 4
+    Wd, _ = _dev_W(W)
+    got = som.som_codebook_norms(Wd, N=777).cpu().numpy()
+    assert np.array_equal(got.astype(np.float64), oracle.codebook_norms(W.astype(np.float64)))
+
+
+# ----------------------------------------------------------------------------
+# exact cases: hand-worked examples and dyadic codebooks
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T", TILES)
+def test_hand_examples_bit_exact(T):
+    ex_all = json.load(open(os.path.join(GOLDEN, "hand_examples.json")))["examples"]
+    for ex in ex_all:
+        F, N = ex["F"], ex["N"]
+        W = np.zeros((F, N), np.float32)
+        for j, w in enumerate(ex["neurons"]):
+            for f, v in enumerate(w):
+                W[f, j] = float(Fraction(v))
+        docs = [d["features"] for d in ex["docs"]]
+        indptr, indices = _csr(docs)
+        bmu, dist, norms = _search(W, indptr, indices, tile_docs=T)
+        assert norms.tolist() == [float(Fraction(v)) for v in ex["norms"]]
+        assert bmu.tolist() == [d["bmu"] for d in ex["docs"]]
+        assert dist.tolist() == [float(Fraction(d["d"][d["bmu"]])) for d in ex["docs"]]
+
+
+@pytest.mark.parametrize("N", [1, 3, 5, 63, 511, 513, 1023, 1025, 2065, 5000])
+def test_dyadic_codebook_bit_exact_with_ties(N):
+    """W in {0, 1/4, 1/2, 3/4}: every fp32 sum is exact, so indices (lowest on
+    ties) and distances must equal the exact integer evaluation."""
+    rng = np.random.default_rng(N)
+    F, B = 64, 301
+    K = rng.integers(0, 4, (F, N))
+    if N > 8:
+        K[:, N - 1] = K[:, 2]          # exact duplicate neurons -> ties
+        K[:, N // 2] = K[:, 5]
+    W = K.astype(np.float32) / 4
+    docs = _random_docs(rng, B, F, mean=12, empty_every=17, big_every=50, big=60)
+    indptr, indices = _csr(docs)
+    exact = oracle.bmu_search_exact(K, 2, indptr, indices)
+    for T in (1, 8, 32):
+        bmu, dist, _ = _search(W, indptr, indices, tile_docs=T)
+        assert bmu.tolist() == [e[2][0] for e in exact]
+        assert [Fraction(float(x)) for x in dist] == [Fraction(e[1], 16) for e in exact]
+
+
+# ----------------------------------------------------------------------------
+# tile plan and clustering: integer work, bit-exact
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T", TILES)
+def test_tile_plan_bit_exact(T):
+    from synth import documents
+    indptr, indices = documents(1, 0, n_docs=1001)      # ragged last tile
+    rng = np.random.default_rng(T)
+    for perm in (None, rng.permutation(1001)):
+        off, cnt, uf, um = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), 2048, T,
+                                             perm=None if perm is None else _dev_i32(perm))
+        off, cnt, uf, um = (x.cpu().numpy() for x in (off, cnt, uf, um))
+        tiles = oracle.tile_union(indptr, indices, T, perm)
+        assert len(cnt) == len(tiles)
+        order = np.arange(1001) if perm is None else perm
+        nnz_doc = np.diff(indptr)[order]
+        assert off.tolist() == [0] + np.cumsum([nnz_doc[t * T:(t + 1) * T].sum() for t in range(len(tiles))]).tolist()
+        for t, (feats, masks) in enumerate(tiles):
+            assert cnt[t] == len(feats)
+            assert uf[off[t]:off[t] + cnt[t]].tolist() == feats.tolist()
+            assert um[off[t]:off[t] + cnt[t]].view(np.uint32).tolist() == masks.astype(np.uint32).tolist()
+
+
+def test_tile_plan_large_feature_ids_use_several_windows():
+    rng = np.random.default_rng(3)
+    F = 70_000                                         # > one 32768-feature window
+    docs = _random_docs(rng, 130, F, mean=30, empty_every=9)
+    indptr, indices = _csr(docs)
+    off, cnt, uf, um = (x.cpu().numpy() for x in som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), F, 4))
+    for t, (feats, masks) in enumerate(oracle.tile_union(indptr, indices, 4)):
+        assert uf[off[t]:off[t] + cnt[t]].tolist() == feats.tolist()
+        assert um[off[t]:off[t] + cnt[t]].view(np.uint32).tolist() == masks.astype(np.uint32).tolist()
+
+
+def test_cluster_order_golden():
+    ex_all = json.load(open(os.path.join(GOLDEN, "cluster_examples.json")))["examples"]
+    for ex in ex_all:
+        indptr, indices = _csr(ex["docs"])
+        perm = som.som_cluster_order(_dev_i32(indptr), _dev_i32(indices), ex["F"]).cpu().numpy()
+        assert perm.tolist() == ex["perm"]
+
+
+@pytest.mark.parametrize("cfg,n", [(5, 20000), (2, 8000), (1, 10000)])
+def test_cluster_order_bit_exact(cfg, n):
+    from synth import CONFIGS, documents
+    indptr, indices = documents(cfg, 0, n_docs=n)
+    F = CONFIGS[cfg].F
+    got = som.som_cluster_order(_dev_i32(indptr), _dev_i32(indices), F).cpu().numpy()
+    assert got.tolist() == oracle.cluster_order(indptr, indices, F).tolist()
+
+
+# ----------------------------------------------------------------------------
+# generated workloads under the acceptance rule
+# ----------------------------------------------------------------------------
+
+def _check_docs(W64, norms64, indptr, indices, bmu, dist, docs, N=None):
+    bad = []
+    for d in docs:
+        feats = np.asarray(indices[indptr[d]:indptr[d + 1]], np.int64)
+        ok, why = oracle.accept_bmu(W64, norms64, feats, int(bmu[d]), float(dist[d]), REL, N)
+        if not ok:
+            bad.append((int(d), why))
+    assert not bad, bad[:5]
+
+
+def test_config1_every_document():
+    from synth import codebook, documents
+    W = codebook(1)
+    indptr, indices = documents(1, 0)
+    for T in (1, 4, 8, 32):
+        bmu, dist, _ = _search(W, indptr, indices, tile_docs=T)
+        W64 = W.astype(np.float64)
+        _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, bmu, dist, range(len(indptr) - 1))
+
+
+def test_config2_first_batch():
+    from synth import codebook, documents
+    W = codebook(2)
+    indptr, indices = documents(2, 0)                   # 65,536 documents
+    B = len(indptr) - 1
+    bmu, dist, _ = _search(W, indptr, indices)
+    W64 = W.astype(np.float64)
+    norms64 = oracle.codebook_norms(W64)
+    rng = np.random.default_rng(0)
+    sample = np.unique(np.concatenate([[0, B - 1], rng.choice(B, 1500, replace=False)]))
+    _check_docs(W64, norms64, indptr, indices, bmu, dist, sample)
+    # every document: the reported distance is the distance of the reported neuron
+    nnz = np.diff(indptr)
+    g = np.repeat(bmu, nnz)
+    dot = np.add.reduceat(W64[indices, g], indptr[:-1]) if len(indices) else np.zeros(B)
+    d_at_g = nnz + norms64[bmu] - 2 * dot
+    assert np.all(np.abs(dist - d_at_g) <= REL * np.abs(d_at_g))
+
+
+def test_results_identical_across_tile_chunk_and_order():
+    """Each document's dot product is summed in ascending feature order
+    whatever the tiling, so the outputs are bit-identical."""
+    from synth import codebook, documents
+    W = codebook(2, N=4100, F=20000)
+    indptr, indices = documents(2, 0, n_docs=3000)
+    ref = None
+    rng = np.random.default_rng(5)
+    perms = [None, rng.permutation(3000), oracle.cluster_order(indptr, indices, 20000)]
+    for T in TILES:
+        for chunk in (0, 512 if T < 32 else 256, 1024 if T < 32 else 512):
+            for perm in perms[:2] if T != 8 else perms:
+                out = _search(W, indptr, indices, perm=perm, tile_docs=T, neuron_chunk=chunk)
+                if ref is None:
+                    ref = out
+                assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (T, chunk)
+
+
+def test_repeated_runs_are_bit_identical():
+    from synth import codebook, documents
+    W = codebook(1)
+    indptr, indices = documents(1, 0)
+    a = _search(W, indptr, indices)
+    for _ in range(3):
+        b = _search(W, indptr, indices)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+# ----------------------------------------------------------------------------
+# edge cases
+# ----------------------------------------------------------------------------
+
+def test_empty_batch_and_empty_documents():
+    rng = np.random.default_rng(9)
+    W = rng.random((10, 33), dtype=np.float32)
+    bmu, dist, _ = _search(W, np.zeros(1, np.int64), np.zeros(0, np.int64))
+    assert bmu.size == 0 and dist.size == 0
+    indptr, indices = _csr([[], [], []])
+    bmu, dist, norms = _search(W, indptr, indices)
+    first = int(np.argmin(oracle.codebook_norms(W.astype(np.float64))))
+    assert bmu.tolist() == [first] * 3
+
+
+def test_single_neuron_and_long_documents():
+    rng = np.random.default_rng(10)
+    W = rng.random((5000, 1), dtype=np.float32)
+    docs = _random_docs(rng, 40, 5000, mean=5, big_every=3, big=4000)
+    indptr, indices = _csr(docs)
+    bmu, dist, _ = _search(W, indptr, indices, ldw=4)
+    assert np.all(bmu == 0)
+    W64 = W.astype(np.float64)
+    _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, bmu, dist, range(40))
+
+
+def test_validate_rejects_malformed_batches():
+    rng = np.random.default_rng(11)
+    W = rng.random((50, 64), dtype=np.float32)
+    Wd, _ = _dev_W(W)
+    norms = som.som_codebook_norms(Wd)
+    good_ptr, good_idx = _csr([[1, 4, 9], [2], [], [0, 49]])
+    som.som_bmu_search(Wd, norms, _dev_i32(good_ptr), _dev_i32(good_idx), validate=True)
+    cases = [
+        (good_ptr, np.array([1, 9, 4, 2, 0, 49])),            # unsorted
+        (good_ptr, np.array([1, 4, 4, 2, 0, 49])),            # duplicate
+        (good_ptr, np.array([1, 4, 9, 2, 0, 50])),            # out of range
+        (good_ptr, np.array([1, 4, 9, 2, -1, 49])),           # negative
+        (np.array([0, 3, 2, 4, 6]), good_idx),                # indptr decreases
+    ]
+    for ip, ix in cases:
+        with pytest.raises(som.SomError) as e:
+            som.som_bmu_search(Wd, norms, _dev_i32(ip), _dev_i32(ix), validate=True)
+        assert e.value.status == 2
+    with pytest.raises(som.SomError) as e:
+        som.som_bmu_search(Wd, norms, _dev_i32(good_ptr), _dev_i32(good_idx),
+                           perm=_dev_i32(np.array([0, 1, 1, 3])), validate=True)
+    assert e.value.status == 2
