@@ -1,0 +1,210 @@
+#!/usr/bin/env python3
+"""Benchmark of the BMU search hot path on one MI355X.
+
+One step = one pass of the whole path over one CSR batch resident in HBM:
+codebook norms, tile-membership clustering, tile plan, fused tiled search
+with the chunk merge.  Default workload: the 512x512 map (N = 262,144
+neurons, F = 20,000 features, fp32 feature-major codebook, 21 GB) against
+the first 1,048,576-document batch of the 2,000,000-document Poisson(80),
+Zipf(1.1) pass.  Prints one JSON line (rank 0).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+L2_PEAK_BPS = 8 * 16 * 128 * 2.4e9       # 8 XCDs x 16 channels x 128 B/clk x 2.4 GHz
+VALU_PEAK_ADDS = 256 * 128 * 2.4e9       # 256 CUs x 128 fp32 lanes/clk x 2.4 GHz
+HBM_PEAK_BPS = 8.0e12
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=3)
+    p.add_argument("--warmup", type=int, default=1)
+    p.add_argument("--config", type=int, default=4, help="workload (1..5)")
+    p.add_argument("--batch", type=int, default=0)
+    p.add_argument("--docs", type=int, default=0, help="override documents per batch (0 = config)")
+    p.add_argument("--tile-docs", type=int, default=0)
+    p.add_argument("--neuron-chunk", type=int, default=0)
+    p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage")
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
+    p.add_argument("--check-docs", type=int, default=64, help="documents checked against the oracle")
+    p.add_argument("--quiet", action="store_true")
+    return p.parse_args()
+
+
+def log(args, *a):
+    if not args.quiet:
+        print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    import paper_2609_05138_amd as som
+    from synth import CONFIGS, batch_sizes, codebook, documents
+
+    if not torch.cuda.is_available():
+        raise SystemExit("no ROCm device visible: the benchmark needs an MI355X")
+    som.load()
+    dev = torch.device("cuda:0")
+    cfg = CONFIGS[args.config]
+    N, F = cfg.N, cfg.F
+    B = args.docs or batch_sizes(cfg)[args.batch]
+
+    t = time.time()
+    W = codebook(cfg)                                    # [F, N] float32, ldw = N
+    log(args, f"codebook {F}x{N} generated in {time.time() - t:.1f}s")
+    t = time.time()
+    indptr, indices = documents(cfg, args.batch, n_docs=B if args.docs else None)
+    nnz = int(indices.size)
+    log(args, f"{B} documents, nnz={nnz} generated in {time.time() - t:.1f}s")
+
+    Wd = torch.from_numpy(W).to(dev)
+    ip = torch.from_numpy(indptr).to(dev)
+    ix = torch.from_numpy(indices).to(dev)
+    norms = torch.empty(N, dtype=torch.float32, device=dev)
+    bmu = torch.empty(B, dtype=torch.int32, device=dev)
+    dist = torch.empty(B, dtype=torch.float32, device=dev)
+    perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
+    T = args.tile_docs or 8
+    cl_ws = torch.empty(max(som.som_cluster_workspace_bytes(B, F, nnz), 1), dtype=torch.uint8, device=dev)
+    s_ws = torch.empty(max(som.som_bmu_search_planned_workspace_bytes(N, B, T, args.neuron_chunk), 1),
+                       dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        som.som_codebook_norms(Wd, N=N, norms=norms)
+        if ev:
+            ev[1].record(stream)
+        if perm is not None:
+            som.som_cluster_order(ip, ix, F, perm=perm, ws=cl_ws)
+        if ev:
+            ev[2].record(stream)
+        plan = som.som_tile_plan(ip, ix, F, T, perm=perm)
+        if ev:
+            ev[3].record(stream)
+        som.som_bmu_search_planned(Wd, norms, ip, plan, N=N, neuron_chunk=args.neuron_chunk,
+                                   bmu=bmu, dist=dist, ws=s_ws)
+        if ev:
+            ev[4].record(stream)
+        return plan
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(args, "warm-up done")
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        plan = step(events[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    stage = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in events])
+    st = stage.mean(axis=0)
+    log(args, f"step {ms_step:.2f} ms; norms {st[0]:.3f} cluster {st[1]:.3f} plan {st[2]:.3f} search {st[3]:.3f} ms")
+
+    union_total = int(plan.tile_count.to(torch.int64).sum().item())
+    ntiles = (B + T - 1) // T
+    pairs = B * N
+    value = pairs / (ms_step * 1e-3)
+    search_s = st[3] * 1e-3
+    # algorithmic L2-level bytes of one search launch: every union row slice
+    # once per tile, plus the norms once per tile
+    l2_bytes = 4.0 * N * (union_total + ntiles)
+    useful_adds = float(nnz) * N
+
+    # spot check of this run's results against the oracle
+    import oracle
+    bmu_h = bmu.cpu().numpy()
+    dist_h = dist.cpu().numpy()
+    t = time.time()
+    norms64 = oracle.codebook_norms_blocks(W[a:a + 500] for a in range(0, F, 500))
+    oracle_norm_s = time.time() - t
+    rng = np.random.default_rng(1234)
+    check = np.unique(np.concatenate([[0, B - 1], rng.choice(B, min(B, args.check_docs), replace=False)]))
+    bad = 0
+    for d in check:
+        feats = indices[indptr[d]:indptr[d + 1]].astype(np.int64)
+        ok, why = oracle.accept_bmu(W, norms64, feats, int(bmu_h[d]), float(dist_h[d]))
+        if not ok:
+            bad += 1
+            log(args, f"doc {d}: {why}")
+    log(args, f"oracle check: {len(check) - bad}/{len(check)} documents accepted")
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        t = time.time()
+        done = 0
+        order = rng.permutation(B)
+        while time.time() - t < args.cpu_seconds and done < B:
+            chunk = order[done:done + 8]
+            oracle.bmu_search(W, indptr, indices, norms=norms64, docs=chunk)
+            done += len(chunk)
+        el = time.time() - t
+        cpu = {"value": done * N / el, "unit": "pairs/s", "cores": 1, "kind": "oracle",
+               "sample": f"{done} random documents of this batch searched by the fp64 oracle "
+                         f"(single-threaded numpy) against all {N} neurons in {el:.1f}s; "
+                         f"its fp64 norms pass ({oracle_norm_s:.1f}s) excluded"}
+
+    out = {
+        "metric": "doc-neuron pairs scored/sec",
+        "value": value,
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name}: map {int(round(N ** 0.5))}^2 (N={N}), F={F}, fp32 feature-major codebook; "
+                         f"batch {args.batch}: {B} binary documents, nnz={nnz}"),
+            "N": N, "F": F, "B": B, "nnz": nnz, "tile_docs": T,
+            "neuron_chunk": args.neuron_chunk or "auto", "clustered": perm is not None,
+            "bmu_pass_ms": float(st[1] + st[2] + st[3]),
+        },
+        "roofline": {
+            "kernel": "search (fused tiled sweep + argmin, chunk merge)",
+            "bound": "l2",
+            "achieved": l2_bytes / search_s / 1e9,
+            "peak": L2_PEAK_BPS / 1e9,
+            "unit": "GB/s",
+            "frac": (l2_bytes / search_s) / L2_PEAK_BPS,
+            "traffic": None,
+            "algorithmic_bytes": l2_bytes,
+            "union_per_doc": union_total / B,
+            "alu_useful_adds_frac": useful_adds / search_s / VALU_PEAK_ADDS,
+        },
+        "cpu_baseline": cpu,
+        "stages_ms": {"norms": float(st[0]), "cluster": float(st[1]), "plan": float(st[2]),
+                      "search": float(st[3])},
+        "oracle_check": {"documents": int(len(check)), "rejected": int(bad)},
+    }
+    print(json.dumps(out), flush=True)
+    if bad:
+        sys.exit(1)
+
+
+if __name__ == "__main__":
+    main()

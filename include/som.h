@@ -56,7 +56,8 @@ typedef enum som_status {
  * selects the defaults. */
 typedef struct som_bmu_opts {
   int32_t tile_docs;    /* T, documents per tile (Section 4.1): 0 = auto, else 1, 2, 4, 8, 16 or 32 */
-  int32_t neuron_chunk; /* neurons per partial-argmin chunk (Section 4.2): 0 = auto, else a multiple of 2048 */
+  int32_t neuron_chunk; /* neurons per workgroup and partial-argmin chunk (Section 4.2): 0 = auto,
+                           else 1, 2 or 4 waves of 64*K neurons (K = 8 for T <= 16, 4 for T = 32) */
   int32_t validate;     /* 1 = check the CSR batch on the device first (synchronises `stream`) */
   int32_t reserved;     /* must be 0 */
 } som_bmu_opts;
@@ -114,14 +115,26 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
  *   tile_count  int32 [ntiles] output: |U_t|
  *   union_feat  int32 [nnz] output (entries past each tile's count are unused)
  *   union_mask  uint32 [nnz] output
- *   ws          at least som_tile_plan_workspace_bytes(B, tile_docs) bytes
- * This is the first stage of som_bmu_search, exported so that it can be
- * checked on its own. */
-size_t som_tile_plan_workspace_bytes(int64_t B, int32_t tile_docs);
+ * Needs no workspace.  The plan depends only on the batch (and perm, T), so
+ * it can be built once and searched against many codebook versions with
+ * som_bmu_search_planned; som_bmu_search runs both stages. */
 som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                          int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,
-                         int32_t* tile_count, int32_t* union_feat, uint32_t* union_mask, void* ws,
-                         size_t ws_bytes, hipStream_t stream);
+                         int32_t* tile_count, int32_t* union_feat, uint32_t* union_mask,
+                         hipStream_t stream);
+
+/* The search stage alone, on a plan from som_tile_plan built from the same
+ * indptr, perm and opts->tile_docs (T; 0 = the default of som_bmu_search).
+ * Arguments as for som_bmu_search; the workspace holds only the per-chunk
+ * partial minima: at least som_bmu_search_planned_workspace_bytes(...). */
+size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bmu_opts* opts);
+som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
+                                  const float* norms, const int32_t* indptr, int64_t B,
+                                  const int32_t* perm, const int32_t* tile_offset,
+                                  const int32_t* tile_count, const int32_t* union_feat,
+                                  const uint32_t* union_mask, int32_t* bmu, float* dist,
+                                  const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                  hipStream_t stream);
 
 /* Tile-membership clustering (Section 4.2: documents that share descriptors
  * are placed in the same tile, shrinking each tile's union).  The paper

@@ -25,6 +25,7 @@ som_status hip_fail(hipError_t e, const char* where) {
 }
 
 constexpr int64_t kI32Max = 2147483647;
+constexpr int64_t kMaxTiles = int64_t(1) << 24;
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -72,15 +73,22 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
   p->waves = waves;
   p->ntiles = (B + T - 1) / T;
   p->nchunks = (N + waves * wave_n - 1) / (waves * wave_n);
-  if (p->ntiles * p->nchunks > kI32Max)
-    return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: ceil(B/T) * chunks must be < 2^31");
+  // one 256-thread plan workgroup per tile, and the search grid (tiles,
+  // chunks): work-items per grid dimension must stay below 2^32
+  if (p->ntiles >= kMaxTiles)
+    return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: ceil(B/T) must be < 2^24");
+  if (p->nchunks > 65535)
+    return fail(SOM_ERR_INVALID_ARG, "too many neuron chunks for one launch (N / neuron_chunk must be <= 65535)");
   return SOM_OK;
 }
 
-// Workspace layout of som_bmu_search (each region 256-byte aligned).
+// Workspace layout of som_bmu_search (each region 256-byte aligned): the
+// tile plan, then the per-chunk partial minima (the planned search's part).
 struct SearchWs {
   size_t tile_offset, tile_count, union_feat, union_mask, partial, flag, seen, total;
 };
+
+size_t partial_bytes(const Plan& p) { return sizeof(uint64_t) * p.nchunks * p.ntiles * p.T; }
 
 SearchWs search_ws(const Plan& p, int64_t B, int64_t nnz, bool validate) {
   SearchWs w{};
@@ -94,9 +102,9 @@ SearchWs search_ws(const Plan& p, int64_t B, int64_t nnz, bool validate) {
   w.tile_count = take(sizeof(int32_t) * p.ntiles);
   w.union_feat = take(sizeof(int32_t) * nnz);
   w.union_mask = take(sizeof(uint32_t) * nnz);
-  w.partial = take(sizeof(uint64_t) * p.nchunks * p.ntiles * p.T);
   w.flag = take(sizeof(int32_t) * 4);
   w.seen = validate ? take(sizeof(int32_t) * B) : 0;
+  w.partial = take(partial_bytes(p));
   w.total = o;
   return w;
 }
@@ -134,6 +142,37 @@ som_status run_validate(const int32_t* indptr, const int32_t* indices, int64_t B
     return fail(SOM_ERR_INVALID_CSR, "invalid batch:" + why);
   }
   return SOM_OK;
+}
+
+som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                       const int32_t* indptr, int64_t B, const int32_t* perm, const int32_t* tile_offset,
+                       const int32_t* tile_count, const int32_t* union_feat, const uint32_t* union_mask,
+                       int32_t* bmu, float* dist, const Plan& p, uint64_t* partial, hipStream_t stream) {
+  som::SearchArgs a{};
+  a.W = W;
+  a.F = F;
+  a.N = N;
+  a.ldw = ldw;
+  a.norms = norms;
+  a.indptr = indptr;
+  a.perm = perm;
+  a.B = B;
+  a.T = p.T;
+  a.waves = p.waves;
+  a.ntiles = p.ntiles;
+  a.nchunks = p.nchunks;
+  a.tile_offset = tile_offset;
+  a.tile_count = tile_count;
+  a.union_feat = union_feat;
+  a.union_mask = union_mask;
+  a.partial = partial;
+  a.bmu = bmu;
+  a.dist = dist;
+  hipError_t e = som::launch_search(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "search launch");
+  e = som::launch_merge(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "merge launch");
+  return ok();
 }
 
 }  // namespace
@@ -187,55 +226,60 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
     s = run_validate(indptr, indices, B, F, nnz, perm, at<int32_t>(ws, w.seen), at<int32_t>(ws, w.flag), stream);
     if (s != SOM_OK) return s;
   }
-  som::SearchArgs a{};
-  a.W = W;
-  a.F = F;
-  a.N = N;
-  a.ldw = ldw;
-  a.norms = norms;
-  a.indptr = indptr;
-  a.perm = perm;
-  a.B = B;
-  a.T = p.T;
-  a.waves = p.waves;
-  a.ntiles = p.ntiles;
-  a.nchunks = p.nchunks;
-  a.tile_offset = at<int32_t>(ws, w.tile_offset);
-  a.tile_count = at<int32_t>(ws, w.tile_count);
-  a.union_feat = at<int32_t>(ws, w.union_feat);
-  a.union_mask = at<uint32_t>(ws, w.union_mask);
-  a.partial = at<uint64_t>(ws, w.partial);
-  a.bmu = bmu;
-  a.dist = dist;
   hipError_t e = som::launch_tile_plan(indptr, indices, B, F, perm, p.T, at<int32_t>(ws, w.tile_offset),
                                        at<int32_t>(ws, w.tile_count), at<int32_t>(ws, w.union_feat),
                                        at<uint32_t>(ws, w.union_mask), stream);
   if (e != hipSuccess) return hip_fail(e, "tile plan launch");
-  e = som::launch_search(a, stream);
-  if (e != hipSuccess) return hip_fail(e, "search launch");
-  e = som::launch_merge(a, stream);
-  if (e != hipSuccess) return hip_fail(e, "merge launch");
-  return ok();
+  return run_planned(W, F, N, ldw, norms, indptr, B, perm, at<int32_t>(ws, w.tile_offset),
+                     at<int32_t>(ws, w.tile_count), at<int32_t>(ws, w.union_feat),
+                     at<uint32_t>(ws, w.union_mask), bmu, dist, p, at<uint64_t>(ws, w.partial), stream);
 }
 
-size_t som_tile_plan_workspace_bytes(int64_t B, int32_t tile_docs) {
-  (void)B;
-  (void)tile_docs;
-  return 0;
+size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bmu_opts* opts) {
+  if (N < 1 || B < 0) return 0;
+  Plan p;
+  if (make_plan(N, B, opts, &p) != SOM_OK) return 0;
+  return som::align_up(partial_bytes(p) ? partial_bytes(p) : 1, 256);
+}
+
+som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
+                                  const float* norms, const int32_t* indptr, int64_t B,
+                                  const int32_t* perm, const int32_t* tile_offset,
+                                  const int32_t* tile_count, const int32_t* union_feat,
+                                  const uint32_t* union_mask, int32_t* bmu, float* dist,
+                                  const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                  hipStream_t stream) {
+  som_status s = check_codebook(W, F, N, ldw);
+  if (s != SOM_OK) return s;
+  if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
+  if (B < 0 || B >= kI32Max) return fail(SOM_ERR_INVALID_ARG, "B must be in [0, 2^31 - 1)");
+  Plan p;
+  s = make_plan(N, B, opts, &p);
+  if (s != SOM_OK) return s;
+  if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on a planned search");
+  if (B == 0) return ok();
+  if (!indptr || !bmu || !dist || !tile_offset || !tile_count || !union_feat || !union_mask)
+    return fail(SOM_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (!ws) return fail(SOM_ERR_WORKSPACE, "ws is NULL");
+  if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
+  if (ws_bytes < partial_bytes(p))
+    return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(partial_bytes(p)) + " bytes");
+  return run_planned(W, F, N, ldw, norms, indptr, B, perm, tile_offset, tile_count, union_feat, union_mask,
+                     bmu, dist, p, static_cast<uint64_t*>(ws), stream);
 }
 
 som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                          int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,
-                         int32_t* tile_count, int32_t* union_feat, uint32_t* union_mask, void* ws,
-                         size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
+                         int32_t* tile_count, int32_t* union_feat, uint32_t* union_mask,
+                         hipStream_t stream) {
   som_status s = check_batch(indptr, indices, B, nnz);
   if (s != SOM_OK) return s;
   if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
   const int T = tile_docs;
   if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
     return fail(SOM_ERR_INVALID_ARG, "tile_docs must be 1, 2, 4, 8, 16 or 32");
+  if ((B + T - 1) / T >= kMaxTiles)
+    return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: ceil(B/T) must be < 2^24");
   if (B == 0) return ok();
   if (!tile_offset || !tile_count || (nnz > 0 && (!union_feat || !union_mask)))
     return fail(SOM_ERR_INVALID_ARG, "an output array is NULL");

@@ -16,8 +16,9 @@
 // merge kernel takes the minimum over chunks and writes results in input
 // order.
 //
-// Workgroups are ordered chunk-major, so the whole device sweeps one neuron
-// chunk at a time and the chunk's columns stay resident in the caches.
+// The grid is (tiles, chunks) with tiles fastest, so workgroups are dispatched
+// chunk-major: the whole device sweeps one neuron chunk at a time and the
+// chunk's columns stay resident in the caches.
 #include "common.h"
 
 namespace som {
@@ -67,9 +68,8 @@ k_search(SearchArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t bid = blockIdx.x;
-  const int64_t c = bid / a.ntiles;
-  const int64_t t = bid - c * a.ntiles;
+  const int64_t t = blockIdx.x;  // tile: fastest-varying, so the grid runs chunk-major
+  const int64_t c = blockIdx.y;  // neuron chunk
   if (threadIdx.x < T) red[threadIdx.x] = kNoKey;
 
   const int64_t n0 = c * CN + wave * WN;  // first neuron of this wave
@@ -171,9 +171,8 @@ __global__ void __launch_bounds__(256) k_merge(SearchArgs a) {
 template <int T, int K, int WAVES>
 hipError_t launch_tkw(const SearchArgs& a, hipStream_t stream) {
   constexpr int U = T <= 8 ? 4 : 2;
-  const int64_t grid = a.ntiles * a.nchunks;
-  hipLaunchKernelGGL((k_search<T, K, WAVES, U>), dim3(static_cast<uint32_t>(grid)), dim3(WAVES * 64),
-                     0, stream, a);
+  const dim3 grid(static_cast<uint32_t>(a.ntiles), static_cast<uint32_t>(a.nchunks));
+  hipLaunchKernelGGL((k_search<T, K, WAVES, U>), grid, dim3(WAVES * 64), 0, stream, a);
   return hipGetLastError();
 }
 

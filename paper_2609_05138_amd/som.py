@@ -28,8 +28,9 @@ EXPORTS = (
     "som_codebook_norms",
     "som_bmu_workspace_bytes",
     "som_bmu_search",
-    "som_tile_plan_workspace_bytes",
     "som_tile_plan",
+    "som_bmu_search_planned_workspace_bytes",
+    "som_bmu_search_planned",
     "som_cluster_workspace_bytes",
     "som_cluster_order",
 )
@@ -79,10 +80,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.som_bmu_search.restype = _i32
     lib.som_bmu_search.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp,
                                    ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
-    lib.som_tile_plan_workspace_bytes.restype = _sz
-    lib.som_tile_plan_workspace_bytes.argtypes = [_i64, _i32]
     lib.som_tile_plan.restype = _i32
-    lib.som_tile_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.som_tile_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp]
+    lib.som_bmu_search_planned_workspace_bytes.restype = _sz
+    lib.som_bmu_search_planned_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(som_bmu_opts)]
+    lib.som_bmu_search_planned.restype = _i32
+    lib.som_bmu_search_planned.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+                                           _vp, _vp, ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
     lib.som_cluster_workspace_bytes.restype = _sz
     lib.som_cluster_workspace_bytes.argtypes = [_i64, _i64, _i64]
     lib.som_cluster_order.restype = _i32
@@ -194,9 +198,22 @@ def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, i
     return bmu, dist
 
 
-def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs: int,
-                  perm: Optional[torch.Tensor] = None, stream=None):
-    """(tile_offset, tile_count, union_feat, union_mask) of the tiled order."""
+class TilePlan:
+    """Device arrays of a tile plan (see som_tile_plan) and how it was built."""
+
+    def __init__(self, tile_offset, tile_count, union_feat, union_mask, tile_docs, B, perm):
+        self.tile_offset = tile_offset
+        self.tile_count = tile_count
+        self.union_feat = union_feat
+        self.union_mask = union_mask
+        self.tile_docs = tile_docs
+        self.B = B
+        self.perm = perm
+
+
+def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs: int = 8,
+                  perm: Optional[torch.Tensor] = None, stream=None) -> TilePlan:
+    """Per-tile feature unions and membership masks of the tiled order."""
     lib = load()
     _dev(indptr, torch.int32, "indptr")
     _dev(indices, torch.int32, "indices")
@@ -211,12 +228,45 @@ def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs
     tile_count = torch.empty(max(ntiles, 1), dtype=torch.int32, device=dev)
     union_feat = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
     union_mask = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
-    ws_bytes = int(lib.som_tile_plan_workspace_bytes(B, T))
-    ws = _workspace(ws_bytes, dev)
     _check(lib.som_tile_plan(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), T, _ptr(tile_offset),
-                             _ptr(tile_count), _ptr(union_feat), _ptr(union_mask), _ptr(ws), ws.numel(),
-                             _stream(stream)))
-    return tile_offset, tile_count[:ntiles], union_feat, union_mask
+                             _ptr(tile_count), _ptr(union_feat), _ptr(union_mask), _stream(stream)))
+    return TilePlan(tile_offset, tile_count[:ntiles], union_feat, union_mask, T, B, perm)
+
+
+def som_bmu_search_planned_workspace_bytes(N: int, B: int, tile_docs=0, neuron_chunk=0) -> int:
+    o = _opts(tile_docs, neuron_chunk, False)
+    return int(load().som_bmu_search_planned_workspace_bytes(N, B, ctypes.byref(o)))
+
+
+def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, plan: TilePlan,
+                           N: Optional[int] = None, neuron_chunk: int = 0,
+                           bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None,
+                           ws: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """The search stage on a prebuilt plan (same indptr and perm)."""
+    lib = load()
+    _dev(W, torch.float32, "W")
+    _dev(norms, torch.float32, "norms")
+    _dev(indptr, torch.int32, "indptr")
+    F, ldw = W.shape
+    n = ldw if N is None else int(N)
+    B = indptr.numel() - 1
+    if B != plan.B:
+        raise ValueError("plan was built for another batch")
+    if bmu is None:
+        bmu = torch.empty(B, dtype=torch.int32, device=W.device)
+    if dist is None:
+        dist = torch.empty(B, dtype=torch.float32, device=W.device)
+    _dev(bmu, torch.int32, "bmu")
+    _dev(dist, torch.float32, "dist")
+    o = _opts(plan.tile_docs, neuron_chunk, False)
+    if ws is None:
+        ws = _workspace(lib.som_bmu_search_planned_workspace_bytes(n, B, ctypes.byref(o)), W.device)
+    _dev(ws, torch.uint8, "ws")
+    _check(lib.som_bmu_search_planned(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), B, _ptr(plan.perm),
+                                      _ptr(plan.tile_offset), _ptr(plan.tile_count), _ptr(plan.union_feat),
+                                      _ptr(plan.union_mask), _ptr(bmu), _ptr(dist), ctypes.byref(o),
+                                      _ptr(ws), ws.numel(), _stream(stream)))
+    return bmu, dist
 
 
 def som_cluster_workspace_bytes(B: int, F: int, nnz: int) -> int:

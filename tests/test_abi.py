@@ -118,11 +118,23 @@ def test_search_rejects_bad_arguments(lib):
 def test_plan_and_cluster_reject_bad_arguments(lib):
     null = None
     fake = ctypes.c_void_p(0x1000)
-    st, msg = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 3, fake, fake, fake, fake, null, 0, null)
+    st, msg = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 3, fake, fake, fake, fake, null)
     assert st == som.SOM_ERR_INVALID_ARG and "tile_docs" in msg
-    st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 0, 10, null, 4, fake, fake, fake, fake, null, 0, null)
+    st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 0, 10, null, 4, fake, fake, fake, fake, null)
     assert st == som.SOM_ERR_INVALID_ARG
-    st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 4, null, fake, fake, fake, null, 0, null)
+    st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 4, null, fake, fake, fake, null)
+    assert st == som.SOM_ERR_INVALID_ARG
+    o = som.som_bmu_opts(4, 0, 0, 0)
+    assert lib.som_bmu_search_planned_workspace_bytes(1024, 100, ctypes.byref(o)) >= 8 * 100
+    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, fake, fake, fake,
+                    fake, fake, fake, ctypes.byref(o), fake, 4, null)
+    assert st == som.SOM_ERR_WORKSPACE
+    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, null, fake, fake,
+                    fake, fake, fake, ctypes.byref(o), fake, 1 << 20, null)
+    assert st == som.SOM_ERR_INVALID_ARG
+    v = som.som_bmu_opts(4, 0, 1, 0)
+    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, fake, fake, fake,
+                    fake, fake, fake, ctypes.byref(v), fake, 1 << 20, null)
     assert st == som.SOM_ERR_INVALID_ARG
     st, _ = _status(lib, "som_cluster_order", fake, fake, 4, 8, 10, null, fake, 1 << 20, null)
     assert st == som.SOM_ERR_INVALID_ARG

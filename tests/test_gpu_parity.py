@@ -153,9 +153,9 @@ def test_tile_plan_bit_exact(T):
     indptr, indices = documents(1, 0, n_docs=1001)      # ragged last tile
     rng = np.random.default_rng(T)
     for perm in (None, rng.permutation(1001)):
-        off, cnt, uf, um = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), 2048, T,
-                                             perm=None if perm is None else _dev_i32(perm))
-        off, cnt, uf, um = (x.cpu().numpy() for x in (off, cnt, uf, um))
+        pl = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), 2048, T,
+                               perm=None if perm is None else _dev_i32(perm))
+        off, cnt, uf, um = (x.cpu().numpy() for x in (pl.tile_offset, pl.tile_count, pl.union_feat, pl.union_mask))
         tiles = oracle.tile_union(indptr, indices, T, perm)
         assert len(cnt) == len(tiles)
         order = np.arange(1001) if perm is None else perm
@@ -172,7 +172,8 @@ def test_tile_plan_large_feature_ids_use_several_windows():
     F = 70_000                                         # > one 32768-feature window
     docs = _random_docs(rng, 130, F, mean=30, empty_every=9)
     indptr, indices = _csr(docs)
-    off, cnt, uf, um = (x.cpu().numpy() for x in som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), F, 4))
+    pl = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), F, 4)
+    off, cnt, uf, um = (x.cpu().numpy() for x in (pl.tile_offset, pl.tile_count, pl.union_feat, pl.union_mask))
     for t, (feats, masks) in enumerate(oracle.tile_union(indptr, indices, 4)):
         assert uf[off[t]:off[t] + cnt[t]].tolist() == feats.tolist()
         assert um[off[t]:off[t] + cnt[t]].view(np.uint32).tolist() == masks.astype(np.uint32).tolist()
@@ -314,3 +315,22 @@ def test_validate_rejects_malformed_batches():
         som.som_bmu_search(Wd, norms, _dev_i32(good_ptr), _dev_i32(good_idx),
                            perm=_dev_i32(np.array([0, 1, 1, 3])), validate=True)
     assert e.value.status == 2
+
+
+def test_planned_search_reuses_a_plan_across_codebooks():
+    from synth import codebook, documents
+    indptr, indices = documents(1, 0, n_docs=2500)
+    ip, ix = _dev_i32(indptr), _dev_i32(indices)
+    perm = _dev_i32(oracle.cluster_order(indptr, indices, 2048))
+    plan = som.som_tile_plan(ip, ix, 2048, 4, perm=perm)
+    for seed in (0, 1):
+        W = codebook(1, seed=seed)
+        Wd, _ = _dev_W(W)
+        norms = som.som_codebook_norms(Wd)
+        a = som.som_bmu_search_planned(Wd, norms, ip, plan)
+        b = som.som_bmu_search(Wd, norms, ip, ix, perm=perm, tile_docs=4)
+        torch.cuda.synchronize()
+        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+        W64 = W.astype(np.float64)
+        _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, a[0].cpu().numpy(),
+                    a[1].cpu().numpy(), range(0, 2500, 7))
