@@ -33,11 +33,15 @@ def parse():
     p.add_argument("--batch", type=int, default=0)
     p.add_argument("--docs", type=int, default=0, help="override documents per batch (0 = config)")
     p.add_argument("--tile-docs", type=int, default=0)
-    p.add_argument("--neuron-chunk", type=int, default=0)
+    p.add_argument("--lane-neurons", type=int, default=0)
+    p.add_argument("--group-tiles", type=int, default=0)
+    p.add_argument("--mask-mode", type=int, default=0)
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     p.add_argument("--check-docs", type=int, default=64, help="documents checked against the oracle")
     p.add_argument("--quiet", action="store_true")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run a device-to-device copy of MIB MiB (for scaling traffic counters)")
     return p.parse_args()
 
 
@@ -58,6 +62,14 @@ def main():
 
     if not torch.cuda.is_available():
         raise SystemExit("no ROCm device visible: the benchmark needs an MI355X")
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n}))
+        return
     som.load()
     dev = torch.device("cuda:0")
     cfg = CONFIGS[args.config]
@@ -80,8 +92,10 @@ def main():
     dist = torch.empty(B, dtype=torch.float32, device=dev)
     perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
     T = args.tile_docs or 8
+    knobs = dict(tile_docs=T, lane_neurons=args.lane_neurons, group_tiles=args.group_tiles,
+                 mask_mode=args.mask_mode)
     cl_ws = torch.empty(max(som.som_cluster_workspace_bytes(B, F, nnz), 1), dtype=torch.uint8, device=dev)
-    s_ws = torch.empty(max(som.som_bmu_search_planned_workspace_bytes(N, B, T, args.neuron_chunk), 1),
+    s_ws = torch.empty(max(som.som_bmu_search_planned_workspace_bytes(N, B, **knobs), 1),
                        dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
@@ -98,8 +112,7 @@ def main():
         plan = som.som_tile_plan(ip, ix, F, T, perm=perm)
         if ev:
             ev[3].record(stream)
-        som.som_bmu_search_planned(Wd, norms, ip, plan, N=N, neuron_chunk=args.neuron_chunk,
-                                   bmu=bmu, dist=dist, ws=s_ws)
+        som.som_bmu_search_planned(Wd, norms, ip, plan, N=N, bmu=bmu, dist=dist, ws=s_ws, **knobs)
         if ev:
             ev[4].record(stream)
         return plan
@@ -181,11 +194,11 @@ def main():
             "workload": (f"{cfg.name}: map {int(round(N ** 0.5))}^2 (N={N}), F={F}, fp32 feature-major codebook; "
                          f"batch {args.batch}: {B} binary documents, nnz={nnz}"),
             "N": N, "F": F, "B": B, "nnz": nnz, "tile_docs": T,
-            "neuron_chunk": args.neuron_chunk or "auto", "clustered": perm is not None,
+            "knobs": {k: (v or "auto") for k, v in knobs.items()}, "clustered": perm is not None,
             "bmu_pass_ms": float(st[1] + st[2] + st[3]),
         },
         "roofline": {
-            "kernel": "search (fused tiled sweep + argmin, chunk merge)",
+            "kernel": "k_search (fused tiled sweep + argmin) with key init and decode",
             "bound": "l2",
             "achieved": l2_bytes / search_s / 1e9,
             "peak": L2_PEAK_BPS / 1e9,

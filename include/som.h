@@ -53,13 +53,18 @@ typedef enum som_status {
 } som_status;
 
 /* Tuning knobs of som_bmu_search.  A zero-initialised struct (or NULL)
- * selects the defaults. */
+ * selects the defaults.  None of them changes a result: every document's
+ * dot product is summed in ascending feature order whatever the knobs. */
 typedef struct som_bmu_opts {
   int32_t tile_docs;    /* T, documents per tile (Section 4.1): 0 = auto, else 1, 2, 4, 8, 16 or 32 */
-  int32_t neuron_chunk; /* neurons per workgroup and partial-argmin chunk (Section 4.2): 0 = auto,
-                           else 1, 2 or 4 waves of 64*K neurons (K = 8 for T <= 16, 4 for T = 32) */
+  int32_t lane_neurons; /* K, neurons per lane (128-bit loads, Section 4.3): 0 = auto, 4 or 8;
+                           one neuron slice (the argmin chunk of Section 4.2) is 64*K neurons;
+                           T = 32 needs K = 4 */
+  int32_t group_tiles;  /* tiles per workgroup, all on one neuron slice: 0 = auto, 1, 2, 4 or 8 */
+  int32_t mask_mode;    /* 0 = auto, 1 = branch-free multiply by the membership bit,
+                           2 = one scalar branch per document */
   int32_t validate;     /* 1 = check the CSR batch on the device first (synchronises `stream`) */
-  int32_t reserved;     /* must be 0 */
+  int32_t reserved[3];  /* must be 0 */
 } som_bmu_opts;
 
 /* Version of this ABI (bumped on any incompatible change). */

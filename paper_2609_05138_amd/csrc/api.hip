@@ -42,53 +42,55 @@ som_status check_codebook(const float* W, int64_t F, int64_t N, int64_t ldw) {
 struct Plan {
   int T = 8;
   int K = 8;
-  int waves = 4;
+  int group = 1;
+  int mask_mode = 1;        // SearchArgs encoding: 0 = fma, 1 = branch
   int64_t ntiles = 0;
   int64_t nchunks = 0;
 };
 
+// Defaults chosen by measurement on MI355X (512^2 map, F = 20,000).
+constexpr int kDefaultT = 8;
+constexpr int kDefaultK = 8;
+constexpr int kDefaultGroup = 1;
+
 som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
   som_bmu_opts o{};
   if (opts) o = *opts;
-  if (o.reserved != 0) return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
+  if (o.reserved[0] || o.reserved[1] || o.reserved[2])
+    return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
   if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
-  int T = o.tile_docs ? o.tile_docs : 8;
+  const int T = o.tile_docs ? o.tile_docs : kDefaultT;
   if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
     return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 1, 2, 4, 8, 16 or 32");
-  const int K = som::lanes_neurons(T);
-  const int64_t wave_n = 64 * K;
-  int waves;
-  if (o.neuron_chunk) {
-    if (o.neuron_chunk < 0 || o.neuron_chunk % wave_n != 0)
-      return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk must be a positive multiple of 64*K (512, or 256 for T=32)");
-    waves = static_cast<int>(o.neuron_chunk / wave_n);
-    if (waves != 1 && waves != 2 && waves != 4)
-      return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk must be 1, 2 or 4 waves of 64*K neurons");
-  } else {
-    const int64_t need = (N + wave_n - 1) / wave_n;
-    waves = need >= 4 ? 4 : (need >= 2 ? 2 : 1);
-  }
+  const int K = o.lane_neurons ? o.lane_neurons : (T >= 32 ? 4 : kDefaultK);
+  if (K != 4 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0, 4 or 8");
+  if (T == 32 && K != 4) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 4 when tile_docs is 32");
+  const int G = o.group_tiles ? o.group_tiles : kDefaultGroup;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles must be 0, 1, 2, 4 or 8");
+  if (o.mask_mode < 0 || o.mask_mode > 2) return fail(SOM_ERR_INVALID_ARG, "opts->mask_mode must be 0, 1 or 2");
   p->T = T;
   p->K = K;
-  p->waves = waves;
+  p->group = G;
+  p->mask_mode = o.mask_mode == 2 ? 1 : (o.mask_mode == 1 ? 0 : (T <= 4 ? 0 : 1));
   p->ntiles = (B + T - 1) / T;
-  p->nchunks = (N + waves * wave_n - 1) / (waves * wave_n);
-  // one 256-thread plan workgroup per tile, and the search grid (tiles,
-  // chunks): work-items per grid dimension must stay below 2^32
+  p->nchunks = (N + 64 * K - 1) / (64 * K);
+  // one 256-thread plan workgroup per tile, and the search grid (tile
+  // groups, slices): work-items per grid dimension must stay below 2^32
   if (p->ntiles >= kMaxTiles)
     return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: ceil(B/T) must be < 2^24");
   if (p->nchunks > 65535)
-    return fail(SOM_ERR_INVALID_ARG, "too many neuron chunks for one launch (N / neuron_chunk must be <= 65535)");
+    return fail(SOM_ERR_INVALID_ARG, "too many neuron slices for one launch (N / (64*K) must be <= 65535)");
   return SOM_OK;
 }
 
 // Workspace layout of som_bmu_search (each region 256-byte aligned): the
-// tile plan, then the per-chunk partial minima (the planned search's part).
+// tile plan, then the per-document packed minima (the planned search's part).
 struct SearchWs {
   size_t tile_offset, tile_count, union_feat, union_mask, partial, flag, seen, total;
 };
 
-size_t partial_bytes(const Plan& p) { return sizeof(uint64_t) * p.nchunks * p.ntiles * p.T; }
+size_t partial_bytes(const Plan& p) { return sizeof(uint64_t) * p.ntiles * p.T; }
 
 SearchWs search_ws(const Plan& p, int64_t B, int64_t nnz, bool validate) {
   SearchWs w{};
@@ -158,14 +160,16 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
   a.perm = perm;
   a.B = B;
   a.T = p.T;
-  a.waves = p.waves;
+  a.K = p.K;
+  a.group = p.group;
+  a.mask_mode = p.mask_mode;
   a.ntiles = p.ntiles;
   a.nchunks = p.nchunks;
   a.tile_offset = tile_offset;
   a.tile_count = tile_count;
   a.union_feat = union_feat;
   a.union_mask = union_mask;
-  a.partial = partial;
+  a.keys = partial;
   a.bmu = bmu;
   a.dist = dist;
   hipError_t e = som::launch_search(a, stream);
@@ -179,7 +183,7 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 1; }
+int32_t som_abi_version(void) { return 3; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 

@@ -56,22 +56,23 @@ struct SearchArgs {
   const int32_t* perm;
   int64_t B;
   int T;            // documents per tile
-  int waves;        // waves per workgroup (each covers 64 * K neurons)
+  int K;            // neurons per lane (4 or 8); a slice is 64 * K neurons
+  int group;        // tiles (waves) per workgroup, all on the same slice
+  int mask_mode;    // 0 = branch-free fma by the membership bit, 1 = scalar branches
   int64_t ntiles;
-  int64_t nchunks;  // neuron chunks = ceil(N / (waves * 64 * K))
+  int64_t nchunks;  // neuron slices = ceil(N / (64 * K))
   const int32_t* tile_offset;
   const int32_t* tile_count;
   const int32_t* union_feat;
   const uint32_t* union_mask;
-  uint64_t* partial;  // [nchunks][ntiles * T]
+  uint64_t* keys;   // [B] packed (distance, index) minima, tiled order
   int32_t* bmu;
   float* dist;
 };
 
-// Neurons per lane for a tile size (VGPR budget: T * K accumulators).
-inline int lanes_neurons(int T) { return T >= 32 ? 4 : 8; }
-
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream);
+// Initialises the keys, then runs the fused search; launch_merge decodes the
+// keys into results in input order.
 hipError_t launch_merge(const SearchArgs& a, hipStream_t stream);
 
 // Clustering.

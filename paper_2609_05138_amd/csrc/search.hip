@@ -1,34 +1,50 @@
 // Fused BMU search (paper, Section 3; levers of Section 4).
 //
-// One workgroup handles one tile of T documents against one chunk of
-// neurons (Section 4.2, neuron-axis chunking).  Each wave owns 64*K
-// consecutive-by-lane neurons of the chunk (K per lane, read as K/4 128-bit
-// loads, Section 4.3) and keeps the T x K partial dot products in VGPRs.
-// It sweeps the tile's feature union once (Section 4.1): every union row
-// slice is loaded once and added into the accumulators of exactly the
-// documents whose membership bit is set, so each document's dot product is
-// summed in ascending feature order whatever T, the chunking or the tile
-// order (bit-identical results across them).  The argmin is fused
-// (Section 3): distances d = (|S| + ||w_j||^2) - 2*dot are formed in
-// registers, reduced per lane, across the wave with shuffles and across the
-// workgroup's waves with an LDS atomic minimum on packed (distance, index)
-// keys; one key per (chunk, document) goes to the partial array, and a
-// merge kernel takes the minimum over chunks and writes results in input
-// order.
+// Work unit: one wave = one tile of T documents x one neuron slice of 64*K
+// neurons (K per lane, read as K/4 128-bit loads, Section 4.3).  The wave
+// keeps the T x K partial dot products in VGPRs and sweeps the tile's
+// feature union once (Section 4.1): each union row slice is loaded once and
+// added into the accumulators of exactly the documents whose membership bit
+// is set, so every document's dot product is summed in ascending feature
+// order whatever T, the slicing or the tile order (bit-identical results).
+// The argmin is fused (Section 3): distances (|S| + ||w_j||^2) - 2*dot are
+// formed in registers and reduced per lane, then across the wave with
+// shuffles; the wave folds its result into the document's packed
+// (distance, index) key with one 64-bit atomic minimum, so the neuron-axis
+// chunks (Section 4.2) are merged without materialising any score block.
 //
-// The grid is (tiles, chunks) with tiles fastest, so workgroups are dispatched
-// chunk-major: the whole device sweeps one neuron chunk at a time and the
-// chunk's columns stay resident in the caches.
+// A workgroup holds G waves on G different tiles of the SAME slice, and the
+// grid is (tile groups, slices) with tile groups fastest: workgroups are
+// dispatched slice-major, so the whole device sweeps one narrow neuron
+// slice at a time and that slice's hot rows stay resident in each XCD's L2.
 #include "common.h"
 
 namespace som {
 namespace {
 
-template <int T, int K>
+// Add one union row slice into the accumulators of the documents whose
+// membership bit is set.  Two equivalent forms (both add the row in the same
+// order, so their results are bit-identical):
+//   kMaskFma:    acc[s] = fma(w, b_s, acc[s]) with b_s = 1.0 or 0.0 taken from
+//                the wave-uniform mask -- branch-free, T*K VALU per row;
+//   kMaskBranch: a wave-uniform scalar branch per document, popcount*K VALU.
+enum MaskMode { kMaskFma = 0, kMaskBranch = 1 };
+
+
+template <int T, int K, int MODE>
 __device__ __forceinline__ void add_row(float (&acc)[T][K], const float4 (&w)[K / 4], uint32_t m) {
 #pragma unroll
   for (int s = 0; s < T; ++s) {
-    if (m & (1u << s)) {  // wave-uniform: a scalar branch, no divergence
+    if (MODE == kMaskFma) {
+      const float b = (m >> s) & 1u ? 1.f : 0.f;
+#pragma unroll
+      for (int q = 0; q < K / 4; ++q) {
+        acc[s][4 * q + 0] = fmaf(w[q].x, b, acc[s][4 * q + 0]);
+        acc[s][4 * q + 1] = fmaf(w[q].y, b, acc[s][4 * q + 1]);
+        acc[s][4 * q + 2] = fmaf(w[q].z, b, acc[s][4 * q + 2]);
+        acc[s][4 * q + 3] = fmaf(w[q].w, b, acc[s][4 * q + 3]);
+      }
+    } else if (m & (1u << s)) {
 #pragma unroll
       for (int q = 0; q < K / 4; ++q) {
         acc[s][4 * q + 0] += w[q].x;
@@ -38,13 +54,6 @@ __device__ __forceinline__ void add_row(float (&acc)[T][K], const float4 (&w)[K 
       }
     }
   }
-}
-
-template <int K>
-__device__ __forceinline__ void load_row(float4 (&w)[K / 4], const float* row, const bool (&in)[K / 4]) {
-#pragma unroll
-  for (int q = 0; q < K / 4; ++q)
-    w[q] = in[q] ? *reinterpret_cast<const float4*>(row + 256 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
@@ -58,130 +67,159 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
   return k;
 }
 
-template <int T, int K, int WAVES, int U>
-__global__ void __launch_bounds__(WAVES * 64)
+// Each wave stages its tile's union list in its own LDS window, kEntryChunk
+// entries (feature id, mask) at a time, then issues its row loads from
+// scalar registers.  The window is padded with (row 0, empty mask) entries
+// so the row pipeline never branches on the list length.
+constexpr int kEntryChunk = 512;
+
+template <int T, int K, int G, int U, int MODE>
+__global__ void __launch_bounds__(G * 64)
 k_search(SearchArgs a) {
   constexpr int Q = K / 4;
   constexpr int64_t WN = 64 * K;
-  constexpr int64_t CN = WAVES * WN;
-  __shared__ unsigned long long red[T];
+  static_assert(kEntryChunk % (2 * U) == 0, "row batches must tile a window");
+  __shared__ int2 ent_all[G][kEntryChunk + 2 * U];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t t = blockIdx.x;  // tile: fastest-varying, so the grid runs chunk-major
-  const int64_t c = blockIdx.y;  // neuron chunk
-  if (threadIdx.x < T) red[threadIdx.x] = kNoKey;
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * G + wave;  // this wave's tile
+  const int64_t c = blockIdx.y;                                  // neuron slice
+  if (t >= a.ntiles) return;                                     // no barriers below
+  int2* ent = ent_all[wave];
+  if (lane < 2 * U) ent[kEntryChunk + lane] = make_int2(0, 0);
 
-  const int64_t n0 = c * CN + wave * WN;  // first neuron of this wave
+  const int64_t n0 = c * WN;
   float acc[T][K];
 #pragma unroll
   for (int s = 0; s < T; ++s)
 #pragma unroll
     for (int k = 0; k < K; ++k) acc[s][k] = 0.f;
 
-  bool in[Q];
+  // byte offsets of this lane's float4s inside a row slice; lanes past the
+  // row end re-read the row's last float4 (in bounds; never reported)
+  uint32_t offb[Q];
 #pragma unroll
-  for (int q = 0; q < Q; ++q) in[q] = n0 + 256 * q + 4 * lane < a.ldw;
+  for (int q = 0; q < Q; ++q) {
+    const int64_t o = 256 * q + 4 * lane;
+    offb[q] = static_cast<uint32_t>(4 * (n0 + o < a.ldw ? o : a.ldw - 4 - n0));
+  }
+  const int32_t u0 = a.tile_offset[t];
+  const int32_t cnt = a.tile_count[t];
+  const float* __restrict__ Wn = a.W + n0;
+  const int64_t ldw = a.ldw;
 
-  if (n0 < a.N) {
-    const int32_t u0 = a.tile_offset[t];
-    const int32_t cnt = a.tile_count[t];
-    const int32_t* __restrict__ uf = a.union_feat + u0;
-    const uint32_t* __restrict__ um = a.union_mask + u0;
-    const float* __restrict__ Wl = a.W + n0 + 4 * lane;
-    int32_t u = 0;
-    for (; u + U <= cnt; u += U) {
-      float4 w[U][Q];
-      uint32_t m[U];
+  float4 wa[U][Q], wb[U][Q];
+  uint32_t ma[U], mb[U];
+  auto fetch = [&](float4 (&w)[U][Q], uint32_t (&m)[U], int i) {
 #pragma unroll
-      for (int r = 0; r < U; ++r) {
-        const int64_t f = __builtin_amdgcn_readfirstlane(uf[u + r]);
-        m[r] = __builtin_amdgcn_readfirstlane(um[u + r]);
-        load_row<K>(w[r], Wl + f * a.ldw, in);
-      }
+    for (int r = 0; r < U; ++r) {
+      const int2 e = ent[i + r];
+      const int32_t f32 = __builtin_amdgcn_readfirstlane(e.x);
+      m[r] = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(e.y));
+      const char* row = reinterpret_cast<const char*>(Wn + static_cast<int64_t>(f32) * ldw);
 #pragma unroll
-      for (int r = 0; r < U; ++r) add_row<T, K>(acc, w[r], m[r]);
+      for (int q = 0; q < Q; ++q) w[r][q] = *reinterpret_cast<const float4*>(row + offb[q]);
     }
-    for (; u < cnt; ++u) {
-      float4 w[Q];
-      const int64_t f = __builtin_amdgcn_readfirstlane(uf[u]);
-      const uint32_t m = __builtin_amdgcn_readfirstlane(um[u]);
-      load_row<K>(w, Wl + f * a.ldw, in);
-      add_row<T, K>(acc, w, m);
+  };
+  auto process = [&](const float4 (&w)[U][Q], const uint32_t (&m)[U]) {
+#pragma unroll
+    for (int r = 0; r < U; ++r) add_row<T, K, MODE>(acc, w[r], m[r]);
+  };
+
+  for (int32_t base = 0; base < cnt; base += kEntryChunk) {
+    // one wave reads and writes its own window: program order suffices
+    for (int i = lane; i < kEntryChunk; i += 64) {
+      const int32_t idx = base + i;
+      ent[i] = idx < cnt ? make_int2(a.union_feat[u0 + idx], static_cast<int>(a.union_mask[u0 + idx]))
+                         : make_int2(0, 0);
+    }
+    const int32_t rem = cnt - base;
+    const int n = rem < kEntryChunk ? rem : kEntryChunk;
+    // two batches of U rows in flight: load batch i+1 while adding batch i;
+    // loads past n read the zero padding (row 0, empty mask).  Scheduling
+    // barriers keep each batch's loads ahead of the adds of the previous one.
+    fetch(wa, ma, 0);
+    for (int i = 0; i < n; i += 2 * U) {
+      fetch(wb, mb, i + U);
+      __builtin_amdgcn_sched_barrier(0);
+      process(wa, ma);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(wa, ma, i + 2 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      process(wb, mb);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
-  __syncthreads();  // red[] initialised
 
-  if (n0 < a.N) {
-    float nrm[K];
+  float nrm[K];
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t j = n0 + 256 * q + 4 * lane + e;
+      nrm[4 * q + e] = j < a.N ? a.norms[j] : 0.f;
+    }
+#pragma unroll
+  for (int s = 0; s < T; ++s) {
+    const int64_t p = t * T + s;
+    if (p >= a.B) break;
+    const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
+    const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
+    float best = 0.f;
+    uint32_t bj = 0xffffffffu;
 #pragma unroll
     for (int q = 0; q < Q; ++q)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int64_t j = n0 + 256 * q + 4 * lane + e;
-        nrm[4 * q + e] = j < a.N ? a.norms[j] : 0.f;
-      }
-#pragma unroll
-    for (int s = 0; s < T; ++s) {
-      const int64_t p = t * T + s;
-      if (p >= a.B) break;
-      const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
-      const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
-      float best = 0.f;
-      uint32_t bj = 0xffffffffu;
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int64_t j = n0 + 256 * q + 4 * lane + e;
-          if (j < a.N) {
-            const float dj = fmaf(-2.f, acc[s][4 * q + e], nnz + nrm[4 * q + e]);
-            if (bj == 0xffffffffu || dj < best) {  // ascending j: strict < keeps the lowest
-              best = dj;
-              bj = static_cast<uint32_t>(j);
-            }
+        if (j < a.N) {
+          const float dj = fmaf(-2.f, acc[s][4 * q + e], nnz + nrm[4 * q + e]);
+          if (bj == 0xffffffffu || dj < best) {  // ascending j: strict < keeps the lowest
+            best = dj;
+            bj = static_cast<uint32_t>(j);
           }
         }
-      uint64_t key = bj == 0xffffffffu ? kNoKey : pack_key(best, bj);
-      key = wave_min_u64(key);
-      if (lane == 0) atomicMin(&red[s], static_cast<unsigned long long>(key));
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x < T) {
-    const int64_t p = t * T + threadIdx.x;
-    if (p < a.B) a.partial[c * (a.ntiles * T) + p] = red[threadIdx.x];
+      }
+    uint64_t key = bj == 0xffffffffu ? kNoKey : pack_key(best, bj);
+    key = wave_min_u64(key);
+    if (lane == 0) atomicMin(reinterpret_cast<unsigned long long*>(a.keys + p), static_cast<unsigned long long>(key));
   }
 }
 
-__global__ void __launch_bounds__(256) k_merge(SearchArgs a) {
+__global__ void __launch_bounds__(256) k_keys_init(uint64_t* __restrict__ keys, int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) keys[i] = kNoKey;
+}
+
+// Decode each document's key into (bmu, dist) in input order.
+__global__ void __launch_bounds__(256) k_decode(SearchArgs a) {
   const int64_t p = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (p >= a.B) return;
-  const int64_t P = a.ntiles * a.T;
-  uint64_t best = kNoKey;
-  for (int64_t c = 0; c < a.nchunks; ++c) {
-    const uint64_t k = a.partial[c * P + p];
-    best = k < best ? k : best;
-  }
+  const uint64_t best = a.keys[p];
   const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
   a.bmu[d] = static_cast<int32_t>(static_cast<uint32_t>(best));
   a.dist[d] = from_ordered_bits(static_cast<uint32_t>(best >> 32));
 }
 
-template <int T, int K, int WAVES>
-hipError_t launch_tkw(const SearchArgs& a, hipStream_t stream) {
-  constexpr int U = T <= 8 ? 4 : 2;
-  const dim3 grid(static_cast<uint32_t>(a.ntiles), static_cast<uint32_t>(a.nchunks));
-  hipLaunchKernelGGL((k_search<T, K, WAVES, U>), grid, dim3(WAVES * 64), 0, stream, a);
+template <int T, int K, int G>
+hipError_t launch_tkg(const SearchArgs& a, hipStream_t stream) {
+  constexpr int U = K == 4 ? 8 : 4;
+  const dim3 grid(static_cast<uint32_t>((a.ntiles + G - 1) / G), static_cast<uint32_t>(a.nchunks));
+  if (a.mask_mode == kMaskBranch)
+    hipLaunchKernelGGL((k_search<T, K, G, U, kMaskBranch>), grid, dim3(G * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_search<T, K, G, U, kMaskFma>), grid, dim3(G * 64), 0, stream, a);
   return hipGetLastError();
 }
 
 template <int T, int K>
 hipError_t launch_tk(const SearchArgs& a, hipStream_t stream) {
-  switch (a.waves) {
-    case 1: return launch_tkw<T, K, 1>(a, stream);
-    case 2: return launch_tkw<T, K, 2>(a, stream);
-    case 4: return launch_tkw<T, K, 4>(a, stream);
+  switch (a.group) {
+    case 1: return launch_tkg<T, K, 1>(a, stream);
+    case 2: return launch_tkg<T, K, 2>(a, stream);
+    case 4: return launch_tkg<T, K, 4>(a, stream);
+    case 8: return launch_tkg<T, K, 8>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -189,19 +227,21 @@ hipError_t launch_tk(const SearchArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(k_keys_init, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream,
+                     a.keys, a.B);
   switch (a.T) {
-    case 1: return launch_tk<1, 8>(a, stream);
-    case 2: return launch_tk<2, 8>(a, stream);
-    case 4: return launch_tk<4, 8>(a, stream);
-    case 8: return launch_tk<8, 8>(a, stream);
-    case 16: return launch_tk<16, 8>(a, stream);
+    case 1: return a.K == 4 ? launch_tk<1, 4>(a, stream) : launch_tk<1, 8>(a, stream);
+    case 2: return a.K == 4 ? launch_tk<2, 4>(a, stream) : launch_tk<2, 8>(a, stream);
+    case 4: return a.K == 4 ? launch_tk<4, 4>(a, stream) : launch_tk<4, 8>(a, stream);
+    case 8: return a.K == 4 ? launch_tk<8, 4>(a, stream) : launch_tk<8, 8>(a, stream);
+    case 16: return a.K == 4 ? launch_tk<16, 4>(a, stream) : launch_tk<16, 8>(a, stream);
     case 32: return launch_tk<32, 4>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_merge(const SearchArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(k_merge, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(k_decode, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

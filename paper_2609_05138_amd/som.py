@@ -45,9 +45,11 @@ class SomError(RuntimeError):
 class som_bmu_opts(ctypes.Structure):
     _fields_ = [
         ("tile_docs", ctypes.c_int32),
-        ("neuron_chunk", ctypes.c_int32),
+        ("lane_neurons", ctypes.c_int32),
+        ("group_tiles", ctypes.c_int32),
+        ("mask_mode", ctypes.c_int32),
         ("validate", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("reserved", ctypes.c_int32 * 3),
     ]
 
 
@@ -121,8 +123,9 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _opts(tile_docs=0, neuron_chunk=0, validate=False) -> som_bmu_opts:
-    return som_bmu_opts(int(tile_docs), int(neuron_chunk), int(bool(validate)), 0)
+def _opts(tile_docs=0, lane_neurons=0, group_tiles=0, mask_mode=0, validate=False) -> som_bmu_opts:
+    return som_bmu_opts(int(tile_docs), int(lane_neurons), int(group_tiles), int(mask_mode),
+                        int(bool(validate)))
 
 
 def _workspace(nbytes: int, device) -> torch.Tensor:
@@ -154,18 +157,19 @@ def som_codebook_norms(W: torch.Tensor, N: Optional[int] = None, norms: Optional
     return norms
 
 
-def som_bmu_workspace_bytes(F: int, N: int, B: int, nnz: int, tile_docs=0, neuron_chunk=0,
-                            validate=False) -> int:
-    o = _opts(tile_docs, neuron_chunk, validate)
+def som_bmu_workspace_bytes(F: int, N: int, B: int, nnz: int, validate=False, **knobs) -> int:
+    o = _opts(validate=validate, **knobs)
     return int(load().som_bmu_workspace_bytes(F, N, B, nnz, ctypes.byref(o)))
 
 
 def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, indices: torch.Tensor,
-                   N: Optional[int] = None, perm: Optional[torch.Tensor] = None, tile_docs: int = 0,
-                   neuron_chunk: int = 0, validate: bool = False, bmu: Optional[torch.Tensor] = None,
-                   dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """BMU index (int32) and squared distance (fp32) of every CSR document."""
+                   N: Optional[int] = None, perm: Optional[torch.Tensor] = None, validate: bool = False,
+                   bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None,
+                   ws: Optional[torch.Tensor] = None, stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
+    """BMU index (int32) and squared distance (fp32) of every CSR document.
+
+    ``knobs``: tile_docs, lane_neurons, group_tiles, mask_mode (fields of
+    som_bmu_opts; none changes a result)."""
     lib = load()
     _dev(W, torch.float32, "W")
     _dev(norms, torch.float32, "norms")
@@ -187,7 +191,7 @@ def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, i
     _dev(dist, torch.float32, "dist")
     if bmu.numel() < B or dist.numel() < B:
         raise ValueError("bmu / dist are too small")
-    o = _opts(tile_docs, neuron_chunk, validate)
+    o = _opts(validate=validate, **knobs)
     need = int(lib.som_bmu_workspace_bytes(F, n, B, nnz, ctypes.byref(o)))
     if ws is None:
         ws = _workspace(need, W.device)
@@ -233,15 +237,15 @@ def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs
     return TilePlan(tile_offset, tile_count[:ntiles], union_feat, union_mask, T, B, perm)
 
 
-def som_bmu_search_planned_workspace_bytes(N: int, B: int, tile_docs=0, neuron_chunk=0) -> int:
-    o = _opts(tile_docs, neuron_chunk, False)
+def som_bmu_search_planned_workspace_bytes(N: int, B: int, **knobs) -> int:
+    o = _opts(**knobs)
     return int(load().som_bmu_search_planned_workspace_bytes(N, B, ctypes.byref(o)))
 
 
 def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, plan: TilePlan,
-                           N: Optional[int] = None, neuron_chunk: int = 0,
-                           bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None,
-                           ws: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+                           N: Optional[int] = None, bmu: Optional[torch.Tensor] = None,
+                           dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                           stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
     """The search stage on a prebuilt plan (same indptr and perm)."""
     lib = load()
     _dev(W, torch.float32, "W")
@@ -258,7 +262,10 @@ def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.T
         dist = torch.empty(B, dtype=torch.float32, device=W.device)
     _dev(bmu, torch.int32, "bmu")
     _dev(dist, torch.float32, "dist")
-    o = _opts(plan.tile_docs, neuron_chunk, False)
+    knobs = dict(knobs)
+    if knobs.setdefault("tile_docs", plan.tile_docs) != plan.tile_docs:
+        raise ValueError("tile_docs differs from the plan's")
+    o = _opts(**knobs)
     if ws is None:
         ws = _workspace(lib.som_bmu_search_planned_workspace_bytes(n, B, ctypes.byref(o)), W.device)
     _dev(ws, torch.uint8, "ws")

@@ -42,21 +42,21 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 1
+    assert som.som_abi_version() == 3
 
 
 def test_workspace_sizes_are_host_only(lib):
-    o = som.som_bmu_opts(0, 0, 0, 0)
+    o = som.som_bmu_opts()
     a = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o))
     assert a > 0 and a % 256 == 0
-    # partial keys [chunks][B] dominate: 128 chunks x 1M docs x 8 B
-    assert a >= 128 * (1 << 20) * 8
-    o8 = som.som_bmu_opts(16, 1024, 1, 0)
+    # the plan (two int32 per nonzero) dominates; one packed key per document
+    assert a >= 8 * 84_000_000 + 8 * (1 << 20)
+    o8 = som.som_bmu_opts(16, 8, 4, 0, 1)
     b = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o8))
-    assert b > a
+    assert b > a                   # validation needs a scratch array
     assert lib.som_bmu_workspace_bytes(0, 10, 10, 10, None) == 0
     assert lib.som_bmu_workspace_bytes(10, 10, -1, 10, None) == 0
-    bad = som.som_bmu_opts(3, 0, 0, 0)
+    bad = som.som_bmu_opts(3)
     assert lib.som_bmu_workspace_bytes(10, 10, 10, 10, ctypes.byref(bad)) == 0
 
 
@@ -84,7 +84,7 @@ def test_search_rejects_bad_arguments(lib):
     null = None
     fake = ctypes.c_void_p(0x1000)
     ws_bad = ctypes.c_void_p(0x1010)
-    o = som.som_bmu_opts(0, 0, 0, 0)
+    o = som.som_bmu_opts()
     args = dict(W=fake, F=8, N=8, ldw=8, norms=fake, indptr=fake, indices=fake, B=4, nnz=10,
                 perm=null, bmu=fake, dist=fake, opts=ctypes.byref(o), ws=fake, ws_bytes=1 << 30,
                 stream=null)
@@ -105,9 +105,11 @@ def test_search_rejects_bad_arguments(lib):
     assert st == som.SOM_ERR_WORKSPACE and "need" in msg
     assert call(ws=null)[0] == som.SOM_ERR_WORKSPACE
     assert call(ws=ws_bad)[0] == som.SOM_ERR_INVALID_ARG
-    for bad in (som.som_bmu_opts(3, 0, 0, 0), som.som_bmu_opts(0, 300, 0, 0),
-                som.som_bmu_opts(0, 0, 2, 0), som.som_bmu_opts(0, 0, 0, 1),
-                som.som_bmu_opts(8, 512 * 8, 0, 0)):
+    res = som.som_bmu_opts()
+    res.reserved[1] = 1
+    for bad in (som.som_bmu_opts(3), som.som_bmu_opts(0, 5), som.som_bmu_opts(0, 0, 3), res,
+                som.som_bmu_opts(0, 0, 16), som.som_bmu_opts(0, 0, 0, 3), som.som_bmu_opts(32, 8),
+                som.som_bmu_opts(0, 0, 0, 0, 2), som.som_bmu_opts(0, 0, 0, -1)):
         st, msg = call(opts=ctypes.byref(bad))
         assert st == som.SOM_ERR_INVALID_ARG, msg
     # an empty batch is a valid no-op that touches nothing
@@ -124,7 +126,7 @@ def test_plan_and_cluster_reject_bad_arguments(lib):
     assert st == som.SOM_ERR_INVALID_ARG
     st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 4, null, fake, fake, fake, null)
     assert st == som.SOM_ERR_INVALID_ARG
-    o = som.som_bmu_opts(4, 0, 0, 0)
+    o = som.som_bmu_opts(4)
     assert lib.som_bmu_search_planned_workspace_bytes(1024, 100, ctypes.byref(o)) >= 8 * 100
     st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, fake, fake, fake,
                     fake, fake, fake, ctypes.byref(o), fake, 4, null)
@@ -132,7 +134,7 @@ def test_plan_and_cluster_reject_bad_arguments(lib):
     st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, null, fake, fake,
                     fake, fake, fake, ctypes.byref(o), fake, 1 << 20, null)
     assert st == som.SOM_ERR_INVALID_ARG
-    v = som.som_bmu_opts(4, 0, 1, 0)
+    v = som.som_bmu_opts(4, 0, 0, 0, 1)
     st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, fake, fake, fake,
                     fake, fake, fake, ctypes.byref(v), fake, 1 << 20, null)
     assert st == som.SOM_ERR_INVALID_ARG

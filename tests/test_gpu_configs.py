@@ -1,0 +1,97 @@
+"""GPU parity at the full workload sizes (one batch each), sampled.
+
+For the 256^2 and 512^2 maps (N = 65,536 and 262,144 neurons, F = 20,000,
+codebooks of 5.2 and 21 GB) the oracle cannot score a whole batch, so each
+test runs the device search on a full batch in the launch configuration the
+benchmark uses and checks:
+  * a seeded sample of documents (always including the first and the last)
+    against the fp64 oracle under the acceptance rule, and
+  * every document's reported distance against the fp64 distance of the
+    reported neuron (a property that holds at any size).
+"""
+
+import gc
+
+import numpy as np
+import pytest
+
+import oracle
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2609_05138_amd as som
+else:  # collected on CPU-only machines, never run there
+    som = None
+
+REL = 1e-5
+
+
+def _run(cfg_key, batch, cluster, sample, seed):
+    from synth import CONFIGS, codebook, documents
+    cfg = CONFIGS[cfg_key]
+    dev = torch.device("cuda:0")
+    W = codebook(cfg)
+    indptr, indices = documents(cfg, batch)
+    B = len(indptr) - 1
+    print(f"[cfg{cfg_key} batch {batch}] B={B} nnz={len(indices)} N={cfg.N}", flush=True)
+    Wd = torch.from_numpy(W).to(dev)
+    ip = torch.from_numpy(indptr).to(dev)
+    ix = torch.from_numpy(indices).to(dev)
+    norms = som.som_codebook_norms(Wd)
+    perm = som.som_cluster_order(ip, ix, cfg.F) if cluster else None
+    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, perm=perm)
+    torch.cuda.synchronize()
+    bmu, dist = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
+    if perm is not None:
+        p = perm.cpu().numpy()
+        assert np.array_equal(np.sort(p), np.arange(B))
+    del Wd, ip, ix, norms, perm
+    torch.cuda.empty_cache()
+
+    norms64 = oracle.codebook_norms_blocks(W[a:a + 500] for a in range(0, cfg.F, 500))
+    assert bmu.min() >= 0 and bmu.max() < cfg.N
+    # every document: the distance reported is that of the neuron reported
+    nnz = np.diff(indptr).astype(np.int64)
+    dot = np.zeros(B)
+    for a in range(0, B, 1 << 17):
+        b = min(B, a + (1 << 17))
+        lo, hi = int(indptr[a]), int(indptr[b])
+        g = np.repeat(bmu[a:b], nnz[a:b])
+        vals = W[indices[lo:hi], g].astype(np.float64)
+        starts = (indptr[a:b] - lo).astype(np.int64)
+        part = np.add.reduceat(vals, starts) if hi > lo else np.zeros(b - a)
+        part[nnz[a:b] == 0] = 0.0
+        dot[a:b] = part
+    d_at = nnz + norms64[bmu] - 2.0 * dot
+    assert np.all(np.abs(dist - d_at) <= REL * np.abs(d_at)), "distance does not match its neuron"
+    # sampled documents against the oracle
+    rng = np.random.default_rng(seed)
+    docs = np.unique(np.concatenate([[0, B - 1], rng.choice(B, sample, replace=False)]))
+    bad = []
+    for d in docs:
+        feats = indices[indptr[d]:indptr[d + 1]].astype(np.int64)
+        ok, why = oracle.accept_bmu(W, norms64, feats, int(bmu[d]), float(dist[d]), REL)
+        if not ok:
+            bad.append((int(d), why))
+    print(f"[cfg{cfg_key}] {len(docs) - len(bad)}/{len(docs)} sampled documents accepted", flush=True)
+    del W
+    gc.collect()
+    assert not bad, bad[:5]
+
+
+def test_config3_map256_first_batch():
+    _run(3, 0, cluster=False, sample=300, seed=3)
+
+
+def test_config4_map512_first_batch():
+    _run(4, 0, cluster=False, sample=300, seed=4)
+
+
+def test_config4_map512_ragged_last_batch():
+    _run(4, 1, cluster=True, sample=150, seed=41)
+
+
+def test_config5_topics_clustered_last_batch():
+    _run(5, 26, cluster=True, sample=300, seed=5)

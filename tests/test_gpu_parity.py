@@ -249,12 +249,13 @@ def test_results_identical_across_tile_chunk_and_order():
     rng = np.random.default_rng(5)
     perms = [None, rng.permutation(3000), oracle.cluster_order(indptr, indices, 20000)]
     for T in TILES:
-        for chunk in (0, 512 if T < 32 else 256, 1024 if T < 32 else 512):
+        for K, G, mode in ((0, 0, 0), (4, 1, 1), (8 if T < 32 else 4, 8, 2), (4, 2, 2)):
             for perm in perms[:2] if T != 8 else perms:
-                out = _search(W, indptr, indices, perm=perm, tile_docs=T, neuron_chunk=chunk)
+                out = _search(W, indptr, indices, perm=perm, tile_docs=T, lane_neurons=K, group_tiles=G,
+                              mask_mode=mode)
                 if ref is None:
                     ref = out
-                assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (T, chunk)
+                assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (T, K, G, mode)
 
 
 def test_repeated_runs_are_bit_identical():
