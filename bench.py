@@ -23,6 +23,17 @@ L2_PEAK_BPS = 8 * 16 * 128 * 2.4e9       # 8 XCDs x 16 channels x 128 B/clk x 2.
 VALU_PEAK_ADDS = 256 * 128 * 2.4e9       # 256 CUs x 128 fp32 lanes/clk x 2.4 GHz
 HBM_PEAK_BPS = 8.0e12
 
+# Fabric (MALL/HBM) bytes per search launch measured with rocprofv3 for the
+# default search configuration on the default workload: FETCH_SIZE x 2.0 +
+# WRITE_SIZE x 1.0 (scales from a 4 GiB copy).  Reported only when this run
+# matches that configuration; any kernel change invalidates it.
+MEASURED_TRAFFIC = {
+    ("map512x512-F20000-2M", 0, 1048576, 8, 8, 1, 1): {
+        "bytes": 2.7740e13 + 1.72e10,
+        "source": "profiles/search_map512_1M_counters.md",
+    },
+}
+
 
 def parse():
     p = argparse.ArgumentParser(description=__doc__)
@@ -135,6 +146,10 @@ def main():
     log(args, f"step {ms_step:.2f} ms; norms {st[0]:.3f} cluster {st[1]:.3f} plan {st[2]:.3f} search {st[3]:.3f} ms")
 
     union_total = int(plan.tile_count.to(torch.int64).sum().item())
+    K_eff = args.lane_neurons or (4 if T >= 32 else 8)
+    G_eff = args.group_tiles or 1
+    mode_eff = {1: 0, 2: 1}.get(args.mask_mode, 0 if T <= 4 else 1)
+    measured = MEASURED_TRAFFIC.get((cfg.name, args.batch, B, T, K_eff, G_eff, mode_eff))
     ntiles = (B + T - 1) // T
     pairs = B * N
     value = pairs / (ms_step * 1e-3)
@@ -204,7 +219,9 @@ def main():
             "peak": L2_PEAK_BPS / 1e9,
             "unit": "GB/s",
             "frac": (l2_bytes / search_s) / L2_PEAK_BPS,
-            "traffic": None,
+            "traffic": measured["bytes"] if measured else None,
+            "traffic_source": measured["source"] if measured else None,
+            "traffic_frac_of_hbm_peak": (measured["bytes"] / search_s / HBM_PEAK_BPS) if measured else None,
             "algorithmic_bytes": l2_bytes,
             "union_per_doc": union_total / B,
             "alu_useful_adds_frac": useful_adds / search_s / VALU_PEAK_ADDS,
