@@ -12,6 +12,7 @@ Zipf(1.1) pass.  Prints one JSON line (rank 0).
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -27,12 +28,7 @@ HBM_PEAK_BPS = 8.0e12
 # default search configuration on the default workload: FETCH_SIZE x 2.0 +
 # WRITE_SIZE x 1.0 (scales from a 4 GiB copy).  Reported only when this run
 # matches that configuration; any kernel change invalidates it.
-MEASURED_TRAFFIC = {
-    ("map512x512-F20000-2M", 0, 1048576, 8, 8, 1, 1): {
-        "bytes": 2.7740e13 + 1.72e10,
-        "source": "profiles/search_map512_1M_counters.md",
-    },
-}
+MEASURED_TRAFFIC = {}
 
 
 def parse():
@@ -43,10 +39,12 @@ def parse():
     p.add_argument("--config", type=int, default=4, help="workload (1..5)")
     p.add_argument("--batch", type=int, default=0)
     p.add_argument("--docs", type=int, default=0, help="override documents per batch (0 = config)")
+    p.add_argument("--kernel", type=int, default=0, help="0 auto, 1 neurons on lanes, 2 documents on lanes")
     p.add_argument("--tile-docs", type=int, default=0)
     p.add_argument("--lane-neurons", type=int, default=0)
     p.add_argument("--group-tiles", type=int, default=0)
     p.add_argument("--mask-mode", type=int, default=0)
+    p.add_argument("--slice-neurons", type=int, default=0)
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     p.add_argument("--check-docs", type=int, default=64, help="documents checked against the oracle")
@@ -102,12 +100,16 @@ def main():
     bmu = torch.empty(B, dtype=torch.int32, device=dev)
     dist = torch.empty(B, dtype=torch.float32, device=dev)
     perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
-    T = args.tile_docs or 8
-    knobs = dict(tile_docs=T, lane_neurons=args.lane_neurons, group_tiles=args.group_tiles,
-                 mask_mode=args.mask_mode)
+    knobs = dict(kernel=args.kernel, tile_docs=args.tile_docs, lane_neurons=args.lane_neurons,
+                 group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons)
+    kernel = args.kernel or 2
+    # documents that share one sweep of a union: a kernel-1 tile or a kernel-2 group
+    T = (args.tile_docs or 8) if kernel == 1 else 64 * (args.group_tiles or 16)
     cl_ws = torch.empty(max(som.som_cluster_workspace_bytes(B, F, nnz), 1), dtype=torch.uint8, device=dev)
     s_ws = torch.empty(max(som.som_bmu_search_planned_workspace_bytes(N, B, **knobs), 1),
                        dtype=torch.uint8, device=dev)
+    plan_buf = torch.empty(max(som.load().som_plan_bytes(B, nnz, ctypes.byref(som.som._opts(**knobs))), 1),
+                           dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -120,10 +122,10 @@ def main():
             som.som_cluster_order(ip, ix, F, perm=perm, ws=cl_ws)
         if ev:
             ev[2].record(stream)
-        plan = som.som_tile_plan(ip, ix, F, T, perm=perm)
+        plan = som.som_plan(ip, ix, F, perm=perm, plan=plan_buf, **knobs)
         if ev:
             ev[3].record(stream)
-        som.som_bmu_search_planned(Wd, norms, ip, plan, N=N, bmu=bmu, dist=dist, ws=s_ws, **knobs)
+        som.som_bmu_search_planned(Wd, norms, ip, plan, N=N, bmu=bmu, dist=dist, ws=s_ws)
         if ev:
             ev[4].record(stream)
         return plan
@@ -145,17 +147,19 @@ def main():
     st = stage.mean(axis=0)
     log(args, f"step {ms_step:.2f} ms; norms {st[0]:.3f} cluster {st[1]:.3f} plan {st[2]:.3f} search {st[3]:.3f} ms")
 
-    union_total = int(plan.tile_count.to(torch.int64).sum().item())
-    K_eff = args.lane_neurons or (4 if T >= 32 else 8)
-    G_eff = args.group_tiles or 1
-    mode_eff = {1: 0, 2: 1}.get(args.mask_mode, 0 if T <= 4 else 1)
-    measured = MEASURED_TRAFFIC.get((cfg.name, args.batch, B, T, K_eff, G_eff, mode_eff))
+    # union sizes of this run's tiles/groups (the plan's per-unit counts)
     ntiles = (B + T - 1) // T
+    if kernel == 1:
+        cnt = som.som_tile_plan(ip, ix, F, T, perm=perm)[1]
+    else:
+        cnt = som.som_group_plan(ip, ix, F, T, perm=perm)[1]
+    union_total = int(cnt.to(torch.int64).sum().item())
+    measured = MEASURED_TRAFFIC.get((cfg.name, args.batch, B, kernel, json.dumps(knobs, sort_keys=True)))
     pairs = B * N
     value = pairs / (ms_step * 1e-3)
     search_s = st[3] * 1e-3
     # algorithmic L2-level bytes of one search launch: every union row slice
-    # once per tile, plus the norms once per tile
+    # once per tile (kernel 1) or group (kernel 2), plus the norms once per unit
     l2_bytes = 4.0 * N * (union_total + ntiles)
     useful_adds = float(nnz) * N
 
@@ -208,12 +212,12 @@ def main():
         "config": {
             "workload": (f"{cfg.name}: map {int(round(N ** 0.5))}^2 (N={N}), F={F}, fp32 feature-major codebook; "
                          f"batch {args.batch}: {B} binary documents, nnz={nnz}"),
-            "N": N, "F": F, "B": B, "nnz": nnz, "tile_docs": T,
+            "N": N, "F": F, "B": B, "nnz": nnz, "docs_per_union_sweep": T,
             "knobs": {k: (v or "auto") for k, v in knobs.items()}, "clustered": perm is not None,
             "bmu_pass_ms": float(st[1] + st[2] + st[3]),
         },
         "roofline": {
-            "kernel": "k_search (fused tiled sweep + argmin) with key init and decode",
+            "kernel": ("k_search_docs" if kernel == 2 else "k_search") + " (fused union sweep + argmin) with key init and decode",
             "bound": "l2",
             "achieved": l2_bytes / search_s / 1e9,
             "peak": L2_PEAK_BPS / 1e9,

@@ -52,19 +52,32 @@ typedef enum som_status {
   SOM_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
 } som_status;
 
-/* Tuning knobs of som_bmu_search.  A zero-initialised struct (or NULL)
- * selects the defaults.  None of them changes a result: every document's
- * dot product is summed in ascending feature order whatever the knobs. */
+/* Tuning knobs of the search.  A zero-initialised struct (or NULL) selects
+ * the defaults.  None of them changes a result: every document's dot product
+ * is summed in ascending feature order whatever the knobs, so outputs are
+ * bit-identical across all settings.
+ *
+ * kernel 1, neurons on lanes: a wave holds a tile of T documents (Section
+ *   4.1) against 64*K neurons (K per lane, 128-bit loads, Section 4.3) and
+ *   sweeps the tile's union once, adding each row into the documents whose
+ *   membership bit is set;
+ * kernel 2, documents on lanes: a workgroup holds a group of 64*G documents,
+ *   one per lane, against a narrow slice of NB neurons; the group's feature
+ *   union (the tile union with a tile of 64*G documents) streams through LDS
+ *   and each lane adds the rows of its own document's features.
+ * Either way the neuron axis is cut into slices whose minima are merged
+ * (Section 4.2) and the argmin is fused (Section 3). */
 typedef struct som_bmu_opts {
-  int32_t tile_docs;    /* T, documents per tile (Section 4.1): 0 = auto, else 1, 2, 4, 8, 16 or 32 */
-  int32_t lane_neurons; /* K, neurons per lane (128-bit loads, Section 4.3): 0 = auto, 4 or 8;
-                           one neuron slice (the argmin chunk of Section 4.2) is 64*K neurons;
-                           T = 32 needs K = 4 */
-  int32_t group_tiles;  /* tiles per workgroup, all on one neuron slice: 0 = auto, 1, 2, 4 or 8 */
-  int32_t mask_mode;    /* 0 = auto, 1 = branch-free multiply by the membership bit,
-                           2 = one scalar branch per document */
-  int32_t validate;     /* 1 = check the CSR batch on the device first (synchronises `stream`) */
-  int32_t reserved[3];  /* must be 0 */
+  int32_t kernel;        /* 0 = auto, 1 = neurons on lanes, 2 = documents on lanes */
+  int32_t tile_docs;     /* kernel 1: T = 0 (auto), 1, 2, 4, 8, 16 or 32 */
+  int32_t lane_neurons;  /* kernel 1: K = 0 (auto), 4 or 8; T = 32 needs 4 */
+  int32_t group_tiles;   /* kernel 1: tiles per workgroup, 0 (auto), 1, 2, 4 or 8;
+                            kernel 2: waves per workgroup G, 0 (auto), 4, 8 or 16 */
+  int32_t mask_mode;     /* kernel 1: 0 = auto, 1 = branch-free multiply by the membership
+                            bit, 2 = one scalar branch per document */
+  int32_t slice_neurons; /* kernel 2: NB = 0 (auto), 32 or 64 */
+  int32_t validate;      /* 1 = check the CSR batch on the device first (synchronises `stream`) */
+  int32_t reserved;      /* must be 0 */
 } som_bmu_opts;
 
 /* Version of this ABI (bumped on any incompatible change). */
@@ -87,10 +100,9 @@ som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw,
 size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
                                const som_bmu_opts* opts);
 
-/* BMU of each document of a CSR batch (Section 3; tiles of documents sweep
- * the union of their features once, Section 4.1; the neuron axis is cut
- * into chunks whose partial minima are merged, Section 4.2; the argmin is
- * fused, never materialising the document x neuron score block).
+/* BMU of each document of a CSR batch (Section 3; the tiled sweep of Section
+ * 4.1, the chunked neuron axis of Section 4.2; the argmin is fused, never
+ * materialising the document x neuron score block).
  *   W       fp32 [F][ldw] feature-major codebook (as for som_codebook_norms)
  *   norms   fp32 [N] from som_codebook_norms of the same W
  *   indptr  int32 [B+1], indices int32 [nnz]: the batch (see conventions)
@@ -109,10 +121,31 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
                           const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Tile plan (Section 4.1): for each tile of T consecutive documents of the
- * tiled order (perm as in som_bmu_search; the last tile may be short) the
- * sorted union of their features and, per union entry, a T-bit membership
- * mask (bit s set iff the tile's s-th document contains the feature).
+/* The two stages of som_bmu_search, for callers that search one batch against
+ * several codebook versions (a training loop): the plan depends only on the
+ * batch, perm and opts, never on the codebook.
+ *   som_plan            builds the plan into `plan` (device memory of at least
+ *                       som_plan_bytes(B, nnz, opts) bytes, 256-byte aligned)
+ *   som_bmu_search_planned  searches with it; indptr, perm and opts must be those
+ *                       the plan was built with; ws holds the per-document
+ *                       packed minima (som_bmu_search_planned_workspace_bytes) */
+size_t som_plan_bytes(int64_t B, int64_t nnz, const som_bmu_opts* opts);
+som_status som_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                    int64_t nnz, const int32_t* perm, const som_bmu_opts* opts, void* plan,
+                    size_t plan_bytes, hipStream_t stream);
+size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bmu_opts* opts);
+som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
+                                  const float* norms, const int32_t* indptr, int64_t B,
+                                  int64_t nnz, const int32_t* perm, const void* plan,
+                                  size_t plan_bytes, int32_t* bmu, float* dist,
+                                  const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                  hipStream_t stream);
+
+/* Tile plan of kernel 1 (Section 4.1), written to explicit arrays: for each
+ * tile of T consecutive documents of the tiled order (perm as in
+ * som_bmu_search; the last tile may be short) the sorted union of their
+ * features and, per union entry, a T-bit membership mask (bit s set iff the
+ * tile's s-th document contains the feature).
  *   tile_docs   T in {1, 2, 4, 8, 16, 32}
  *   tile_offset int32 [ntiles+1] output, ntiles = ceil(B / T): tile t's union
  *               is stored at [tile_offset[t], tile_offset[t] + tile_count[t]);
@@ -120,26 +153,26 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
  *   tile_count  int32 [ntiles] output: |U_t|
  *   union_feat  int32 [nnz] output (entries past each tile's count are unused)
  *   union_mask  uint32 [nnz] output
- * Needs no workspace.  The plan depends only on the batch (and perm, T), so
- * it can be built once and searched against many codebook versions with
- * som_bmu_search_planned; som_bmu_search runs both stages. */
+ * Needs no workspace. */
 som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                          int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,
                          int32_t* tile_count, int32_t* union_feat, uint32_t* union_mask,
                          hipStream_t stream);
 
-/* The search stage alone, on a plan from som_tile_plan built from the same
- * indptr, perm and opts->tile_docs (T; 0 = the default of som_bmu_search).
- * Arguments as for som_bmu_search; the workspace holds only the per-chunk
- * partial minima: at least som_bmu_search_planned_workspace_bytes(...). */
-size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bmu_opts* opts);
-som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
-                                  const float* norms, const int32_t* indptr, int64_t B,
-                                  const int32_t* perm, const int32_t* tile_offset,
-                                  const int32_t* tile_count, const int32_t* union_feat,
-                                  const uint32_t* union_mask, int32_t* bmu, float* dist,
-                                  const som_bmu_opts* opts, void* ws, size_t ws_bytes,
-                                  hipStream_t stream);
+/* Group plan of kernel 2, written to explicit arrays: for each group of D
+ * consecutive documents of the tiled order (the last may be short) the sorted
+ * union of their features and, for every nonzero, the position of its feature
+ * in its group's union.
+ *   group_docs   D, 1 .. 65536
+ *   group_offset int32 [ngroups+1] output, ngroups = ceil(B / D) (as tile_offset)
+ *   group_count  int32 [ngroups] output: union size
+ *   group_feat   int32 [nnz] output: the unions, group g at group_offset[g]
+ *   entry_pos    int32 [nnz] output, indexed like `indices`
+ * Needs no workspace. */
+som_status som_group_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                          int64_t nnz, const int32_t* perm, int32_t group_docs,
+                          int32_t* group_offset, int32_t* group_count, int32_t* group_feat,
+                          int32_t* entry_pos, hipStream_t stream);
 
 /* Tile-membership clustering (Section 4.2: documents that share descriptors
  * are placed in the same tile, shrinking each tile's union).  The paper

@@ -167,8 +167,8 @@ def tile_union(indptr: np.ndarray, indices: np.ndarray, T: int, perm: Optional[n
 
     Tile t holds documents perm[t*T : (t+1)*T] (identity when perm is None);
     the last tile may be short.  Returns a list of (features int64[U],
-    masks uint64[U]) where bit s of masks[u] is set iff the tile's s-th
-    document contains features[u].
+    masks[U]) where bit s of masks[u] is set iff the tile's s-th document
+    contains features[u] (uint64 for T <= 64, Python ints beyond).
     """
     B = len(indptr) - 1
     order = np.arange(B) if perm is None else np.asarray(perm, dtype=np.int64)
@@ -179,7 +179,7 @@ def tile_union(indptr: np.ndarray, indices: np.ndarray, T: int, perm: Optional[n
             for f in _rows(indptr, indices, int(d)):
                 members[int(f)] = members.get(int(f), 0) | (1 << s)
         feats = np.array(sorted(members), dtype=np.int64)
-        masks = np.array([members[int(f)] for f in feats], dtype=np.uint64)
+        masks = np.array([members[int(f)] for f in feats], dtype=np.uint64 if T <= 64 else object)
         out.append((feats, masks))
     return out
 

@@ -10,11 +10,13 @@ from .som import (  # noqa: F401
     SomError,
     load,
     som_abi_version,
-    TilePlan,
+    Plan,
     som_bmu_search,
     som_bmu_search_planned,
     som_bmu_search_planned_workspace_bytes,
     som_bmu_workspace_bytes,
+    som_group_plan,
+    som_plan,
     som_cluster_order,
     som_cluster_workspace_bytes,
     som_codebook_norms,

@@ -25,9 +25,19 @@ som_status hip_fail(hipError_t e, const char* where) {
 }
 
 constexpr int64_t kI32Max = 2147483647;
-constexpr int64_t kMaxTiles = int64_t(1) << 24;
+constexpr int64_t kMaxTiles = int64_t(1) << 24;  // tiles or groups per launch
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+template <typename P>
+P* at(void* base, size_t off) {
+  return reinterpret_cast<P*>(static_cast<char*>(base) + off);
+}
+
+template <typename P>
+const P* at(const void* base, size_t off) {
+  return reinterpret_cast<const P*>(static_cast<const char*>(base) + off);
+}
 
 som_status check_codebook(const float* W, int64_t F, int64_t N, int64_t ldw) {
   if (!W) return fail(SOM_ERR_INVALID_ARG, "W is NULL");
@@ -39,89 +49,119 @@ som_status check_codebook(const float* W, int64_t F, int64_t N, int64_t ldw) {
   return SOM_OK;
 }
 
-struct Plan {
-  int T = 8;
-  int K = 8;
-  int group = 1;
-  int mask_mode = 1;        // SearchArgs encoding: 0 = fma, 1 = branch
-  int64_t ntiles = 0;
-  int64_t nchunks = 0;
-};
-
-// Defaults chosen by measurement on MI355X (512^2 map, F = 20,000).
-constexpr int kDefaultT = 8;
-constexpr int kDefaultK = 8;
-constexpr int kDefaultGroup = 1;
-
-som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
-  som_bmu_opts o{};
-  if (opts) o = *opts;
-  if (o.reserved[0] || o.reserved[1] || o.reserved[2])
-    return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
-  if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
-  const int T = o.tile_docs ? o.tile_docs : kDefaultT;
-  if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
-    return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 1, 2, 4, 8, 16 or 32");
-  const int K = o.lane_neurons ? o.lane_neurons : (T >= 32 ? 4 : kDefaultK);
-  if (K != 4 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0, 4 or 8");
-  if (T == 32 && K != 4) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 4 when tile_docs is 32");
-  const int G = o.group_tiles ? o.group_tiles : kDefaultGroup;
-  if (G != 1 && G != 2 && G != 4 && G != 8)
-    return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles must be 0, 1, 2, 4 or 8");
-  if (o.mask_mode < 0 || o.mask_mode > 2) return fail(SOM_ERR_INVALID_ARG, "opts->mask_mode must be 0, 1 or 2");
-  p->T = T;
-  p->K = K;
-  p->group = G;
-  p->mask_mode = o.mask_mode == 2 ? 1 : (o.mask_mode == 1 ? 0 : (T <= 4 ? 0 : 1));
-  p->ntiles = (B + T - 1) / T;
-  p->nchunks = (N + 64 * K - 1) / (64 * K);
-  // one 256-thread plan workgroup per tile, and the search grid (tile
-  // groups, slices): work-items per grid dimension must stay below 2^32
-  if (p->ntiles >= kMaxTiles)
-    return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: ceil(B/T) must be < 2^24");
-  if (p->nchunks > 65535)
-    return fail(SOM_ERR_INVALID_ARG, "too many neuron slices for one launch (N / (64*K) must be <= 65535)");
-  return SOM_OK;
-}
-
-// Workspace layout of som_bmu_search (each region 256-byte aligned): the
-// tile plan, then the per-document packed minima (the planned search's part).
-struct SearchWs {
-  size_t tile_offset, tile_count, union_feat, union_mask, partial, flag, seen, total;
-};
-
-size_t partial_bytes(const Plan& p) { return sizeof(uint64_t) * p.ntiles * p.T; }
-
-SearchWs search_ws(const Plan& p, int64_t B, int64_t nnz, bool validate) {
-  SearchWs w{};
-  size_t o = 0;
-  auto take = [&](size_t bytes) {
-    size_t at = o;
-    o = som::align_up(o + (bytes ? bytes : 1), 256);
-    return at;
-  };
-  w.tile_offset = take(sizeof(int32_t) * (p.ntiles + 1));
-  w.tile_count = take(sizeof(int32_t) * p.ntiles);
-  w.union_feat = take(sizeof(int32_t) * nnz);
-  w.union_mask = take(sizeof(uint32_t) * nnz);
-  w.flag = take(sizeof(int32_t) * 4);
-  w.seen = validate ? take(sizeof(int32_t) * B) : 0;
-  w.partial = take(partial_bytes(p));
-  w.total = o;
-  return w;
-}
-
-template <typename P>
-P* at(void* base, size_t off) {
-  return reinterpret_cast<P*>(static_cast<char*>(base) + off);
-}
-
 som_status check_batch(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz) {
   if (B < 0 || B >= kI32Max) return fail(SOM_ERR_INVALID_ARG, "B must be in [0, 2^31 - 1)");
   if (nnz < 0 || nnz > kI32Max) return fail(SOM_ERR_INVALID_ARG, "nnz must be in [0, 2^31)");
   if (B > 0 && !indptr) return fail(SOM_ERR_INVALID_ARG, "indptr is NULL");
   if (nnz > 0 && !indices) return fail(SOM_ERR_INVALID_ARG, "indices is NULL");
   return SOM_OK;
+}
+
+// Resolved knobs.  Defaults chosen by measurement on MI355X (512^2 map,
+// F = 20,000, 1M-document batches).
+struct Plan {
+  int kernel = 2;
+  // kernel 1
+  int T = 8;
+  int K = 8;
+  int mask_mode = 1;  // SearchArgs encoding: 0 = fma, 1 = branch
+  // kernel 1: tiles per workgroup; kernel 2: waves per workgroup
+  int group = 16;
+  // kernel 2
+  int NB = 32;
+  int64_t D = 1024;     // documents per tile (kernel 1) or per group (kernel 2)
+  int64_t nunits = 0;   // tiles or groups
+  int64_t nchunks = 0;  // neuron slices
+};
+
+som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
+  som_bmu_opts o{};
+  if (opts) o = *opts;
+  if (o.reserved != 0) return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
+  if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
+  if (o.kernel < 0 || o.kernel > 2) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1 or 2");
+  const int kernel = o.kernel ? o.kernel : 2;
+  p->kernel = kernel;
+  if (kernel == 1) {
+    const int T = o.tile_docs ? o.tile_docs : 8;
+    if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
+      return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 1, 2, 4, 8, 16 or 32");
+    const int K = o.lane_neurons ? o.lane_neurons : (T >= 32 ? 4 : 8);
+    if (K != 4 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0, 4 or 8");
+    if (T == 32 && K != 4) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 4 when tile_docs is 32");
+    const int G = o.group_tiles ? o.group_tiles : 1;
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+      return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles must be 0, 1, 2, 4 or 8 for kernel 1");
+    if (o.mask_mode < 0 || o.mask_mode > 2) return fail(SOM_ERR_INVALID_ARG, "opts->mask_mode must be 0, 1 or 2");
+    if (o.slice_neurons != 0) return fail(SOM_ERR_INVALID_ARG, "opts->slice_neurons applies to kernel 2 only");
+    p->T = T;
+    p->K = K;
+    p->group = G;
+    p->mask_mode = o.mask_mode == 2 ? 1 : (o.mask_mode == 1 ? 0 : (T <= 4 ? 0 : 1));
+    p->D = T;
+    p->nchunks = (N + 64 * K - 1) / (64 * K);
+  } else {
+    if (o.tile_docs || o.lane_neurons || o.mask_mode)
+      return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs, lane_neurons and mask_mode apply to kernel 1 only");
+    const int G = o.group_tiles ? o.group_tiles : 16;
+    if (G != 4 && G != 8 && G != 16)
+      return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles must be 0, 4, 8 or 16 for kernel 2");
+    const int NB = o.slice_neurons ? o.slice_neurons : 32;
+    if (NB != 32 && NB != 64) return fail(SOM_ERR_INVALID_ARG, "opts->slice_neurons must be 0, 32 or 64");
+    p->group = G;
+    p->NB = NB;
+    p->D = 64 * G;
+    p->nchunks = (N + NB - 1) / NB;
+  }
+  p->nunits = (B + p->D - 1) / p->D;
+  if (p->nunits >= kMaxTiles)
+    return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: too many tiles or groups");
+  if (p->nchunks > 65535)
+    return fail(SOM_ERR_INVALID_ARG, "too many neuron slices for one launch (N / slice width must be <= 65535)");
+  return SOM_OK;
+}
+
+size_t take(size_t& o, size_t bytes) {
+  const size_t a = o;
+  o = som::align_up(o + (bytes ? bytes : 1), 256);
+  return a;
+}
+
+// Plan layout (each region 256-byte aligned): offsets [nunits+1], counts
+// [nunits], union features [nnz], then kernel 1 masks or kernel 2 entry
+// positions [nnz].
+struct PlanLayout {
+  size_t offset, count, feat, extra, total;
+};
+
+PlanLayout plan_layout(const Plan& p, int64_t nnz) {
+  PlanLayout l{};
+  size_t o = 0;
+  l.offset = take(o, sizeof(int32_t) * (p.nunits + 1));
+  l.count = take(o, sizeof(int32_t) * p.nunits);
+  l.feat = take(o, sizeof(int32_t) * nnz);
+  l.extra = take(o, sizeof(int32_t) * nnz);
+  l.total = o;
+  return l;
+}
+
+size_t keys_bytes(int64_t B) { return som::align_up(sizeof(uint64_t) * (B ? B : 1), 256); }
+
+// Workspace of som_bmu_search: the plan, a validation flag and scratch, the keys.
+struct SearchWs {
+  PlanLayout plan;
+  size_t flag, seen, keys, total;
+};
+
+SearchWs search_ws(const Plan& p, int64_t B, int64_t nnz, bool validate) {
+  SearchWs w{};
+  w.plan = plan_layout(p, nnz);
+  size_t o = w.plan.total;
+  w.flag = take(o, sizeof(int32_t) * 4);
+  w.seen = validate ? take(o, sizeof(int32_t) * B) : 0;
+  w.keys = take(o, keys_bytes(B));
+  w.total = o;
+  return w;
 }
 
 som_status run_validate(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
@@ -146,10 +186,22 @@ som_status run_validate(const int32_t* indptr, const int32_t* indices, int64_t B
   return SOM_OK;
 }
 
+hipError_t build_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                      const int32_t* perm, const Plan& p, void* plan, const PlanLayout& l,
+                      hipStream_t stream) {
+  if (p.kernel == 1)
+    return som::launch_tile_plan(indptr, indices, B, F, perm, p.T, at<int32_t>(plan, l.offset),
+                                 at<int32_t>(plan, l.count), at<int32_t>(plan, l.feat),
+                                 at<uint32_t>(plan, l.extra), stream);
+  return som::launch_group_plan(indptr, indices, B, F, perm, static_cast<int>(p.D),
+                                at<int32_t>(plan, l.offset), at<int32_t>(plan, l.count),
+                                at<int32_t>(plan, l.feat), at<int32_t>(plan, l.extra), stream);
+}
+
 som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
-                       const int32_t* indptr, int64_t B, const int32_t* perm, const int32_t* tile_offset,
-                       const int32_t* tile_count, const int32_t* union_feat, const uint32_t* union_mask,
-                       int32_t* bmu, float* dist, const Plan& p, uint64_t* partial, hipStream_t stream) {
+                       const int32_t* indptr, int64_t B, const int32_t* perm, const void* plan,
+                       const PlanLayout& l, int32_t* bmu, float* dist, const Plan& p, uint64_t* keys,
+                       hipStream_t stream) {
   som::SearchArgs a{};
   a.W = W;
   a.F = F;
@@ -159,23 +211,32 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
   a.indptr = indptr;
   a.perm = perm;
   a.B = B;
+  a.kernel = p.kernel;
   a.T = p.T;
   a.K = p.K;
   a.group = p.group;
   a.mask_mode = p.mask_mode;
-  a.ntiles = p.ntiles;
+  a.slice = p.NB;
+  a.ntiles = p.nunits;
   a.nchunks = p.nchunks;
-  a.tile_offset = tile_offset;
-  a.tile_count = tile_count;
-  a.union_feat = union_feat;
-  a.union_mask = union_mask;
-  a.keys = partial;
+  if (p.kernel == 1) {
+    a.tile_offset = at<int32_t>(plan, l.offset);
+    a.tile_count = at<int32_t>(plan, l.count);
+    a.union_feat = at<int32_t>(plan, l.feat);
+    a.union_mask = at<uint32_t>(plan, l.extra);
+  } else {
+    a.group_offset = at<int32_t>(plan, l.offset);
+    a.group_count = at<int32_t>(plan, l.count);
+    a.group_feat = at<int32_t>(plan, l.feat);
+    a.entry_pos = at<int32_t>(plan, l.extra);
+  }
+  a.keys = keys;
   a.bmu = bmu;
   a.dist = dist;
   hipError_t e = som::launch_search(a, stream);
   if (e != hipSuccess) return hip_fail(e, "search launch");
   e = som::launch_merge(a, stream);
-  if (e != hipSuccess) return hip_fail(e, "merge launch");
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
   return ok();
 }
 
@@ -183,7 +244,7 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 3; }
+int32_t som_abi_version(void) { return 4; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -201,8 +262,7 @@ size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz, con
   if (F < 1 || N < 1 || B < 0 || nnz < 0) return 0;
   Plan p;
   if (make_plan(N, B, opts, &p) != SOM_OK) return 0;
-  const bool validate = opts && opts->validate;
-  return search_ws(p, B, nnz, validate).total;
+  return search_ws(p, B, nnz, opts && opts->validate).total;
 }
 
 som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
@@ -225,51 +285,78 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
   if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
   if (ws_bytes < w.total)
     return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(w.total) + " bytes");
-
   if (validate) {
     s = run_validate(indptr, indices, B, F, nnz, perm, at<int32_t>(ws, w.seen), at<int32_t>(ws, w.flag), stream);
     if (s != SOM_OK) return s;
   }
-  hipError_t e = som::launch_tile_plan(indptr, indices, B, F, perm, p.T, at<int32_t>(ws, w.tile_offset),
-                                       at<int32_t>(ws, w.tile_count), at<int32_t>(ws, w.union_feat),
-                                       at<uint32_t>(ws, w.union_mask), stream);
-  if (e != hipSuccess) return hip_fail(e, "tile plan launch");
-  return run_planned(W, F, N, ldw, norms, indptr, B, perm, at<int32_t>(ws, w.tile_offset),
-                     at<int32_t>(ws, w.tile_count), at<int32_t>(ws, w.union_feat),
-                     at<uint32_t>(ws, w.union_mask), bmu, dist, p, at<uint64_t>(ws, w.partial), stream);
+  hipError_t e = build_plan(indptr, indices, B, F, perm, p, ws, w.plan, stream);
+  if (e != hipSuccess) return hip_fail(e, "plan launch");
+  return run_planned(W, F, N, ldw, norms, indptr, B, perm, ws, w.plan, bmu, dist, p,
+                     at<uint64_t>(ws, w.keys), stream);
+}
+
+size_t som_plan_bytes(int64_t B, int64_t nnz, const som_bmu_opts* opts) {
+  if (B < 0 || nnz < 0) return 0;
+  Plan p;
+  if (make_plan(1, B, opts, &p) != SOM_OK) return 0;
+  return plan_layout(p, nnz).total;
+}
+
+som_status som_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                    int64_t nnz, const int32_t* perm, const som_bmu_opts* opts, void* plan,
+                    size_t plan_bytes, hipStream_t stream) {
+  som_status s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
+  if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate applies to som_bmu_search only");
+  Plan p;
+  s = make_plan(1, B, opts, &p);
+  if (s != SOM_OK) return s;
+  const PlanLayout l = plan_layout(p, nnz);
+  if (B == 0) return ok();
+  if (!plan) return fail(SOM_ERR_WORKSPACE, "plan is NULL");
+  if (!aligned(plan, 256)) return fail(SOM_ERR_INVALID_ARG, "plan must be 256-byte aligned");
+  if (plan_bytes < l.total)
+    return fail(SOM_ERR_WORKSPACE, "plan buffer too small: need " + std::to_string(l.total) + " bytes");
+  hipError_t e = build_plan(indptr, indices, B, F, perm, p, plan, l, stream);
+  if (e != hipSuccess) return hip_fail(e, "plan launch");
+  return ok();
 }
 
 size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bmu_opts* opts) {
   if (N < 1 || B < 0) return 0;
   Plan p;
   if (make_plan(N, B, opts, &p) != SOM_OK) return 0;
-  return som::align_up(partial_bytes(p) ? partial_bytes(p) : 1, 256);
+  return keys_bytes(B);
 }
 
 som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
                                   const float* norms, const int32_t* indptr, int64_t B,
-                                  const int32_t* perm, const int32_t* tile_offset,
-                                  const int32_t* tile_count, const int32_t* union_feat,
-                                  const uint32_t* union_mask, int32_t* bmu, float* dist,
+                                  int64_t nnz, const int32_t* perm, const void* plan,
+                                  size_t plan_bytes, int32_t* bmu, float* dist,
                                   const som_bmu_opts* opts, void* ws, size_t ws_bytes,
                                   hipStream_t stream) {
   som_status s = check_codebook(W, F, N, ldw);
   if (s != SOM_OK) return s;
   if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
   if (B < 0 || B >= kI32Max) return fail(SOM_ERR_INVALID_ARG, "B must be in [0, 2^31 - 1)");
+  if (nnz < 0 || nnz > kI32Max) return fail(SOM_ERR_INVALID_ARG, "nnz must be in [0, 2^31)");
+  if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on a planned search");
   Plan p;
   s = make_plan(N, B, opts, &p);
   if (s != SOM_OK) return s;
-  if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on a planned search");
+  const PlanLayout l = plan_layout(p, nnz);
   if (B == 0) return ok();
-  if (!indptr || !bmu || !dist || !tile_offset || !tile_count || !union_feat || !union_mask)
-    return fail(SOM_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (!indptr || !bmu || !dist || !plan) return fail(SOM_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (!aligned(plan, 256)) return fail(SOM_ERR_INVALID_ARG, "plan must be 256-byte aligned");
+  if (plan_bytes < l.total)
+    return fail(SOM_ERR_INVALID_ARG, "plan buffer smaller than this batch's plan: need " + std::to_string(l.total) + " bytes");
   if (!ws) return fail(SOM_ERR_WORKSPACE, "ws is NULL");
   if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
-  if (ws_bytes < partial_bytes(p))
-    return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(partial_bytes(p)) + " bytes");
-  return run_planned(W, F, N, ldw, norms, indptr, B, perm, tile_offset, tile_count, union_feat, union_mask,
-                     bmu, dist, p, static_cast<uint64_t*>(ws), stream);
+  if (ws_bytes < keys_bytes(B))
+    return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(keys_bytes(B)) + " bytes");
+  return run_planned(W, F, N, ldw, norms, indptr, B, perm, plan, l, bmu, dist, p,
+                     static_cast<uint64_t*>(ws), stream);
 }
 
 som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
@@ -293,15 +380,33 @@ som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t 
   return ok();
 }
 
+som_status som_group_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                          int64_t nnz, const int32_t* perm, int32_t group_docs,
+                          int32_t* group_offset, int32_t* group_count, int32_t* group_feat,
+                          int32_t* entry_pos, hipStream_t stream) {
+  som_status s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
+  if (group_docs < 1 || group_docs > 65536) return fail(SOM_ERR_INVALID_ARG, "group_docs must be in [1, 65536]");
+  if ((B + group_docs - 1) / group_docs >= kMaxTiles)
+    return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: too many groups");
+  if (B == 0) return ok();
+  if (!group_offset || !group_count || (nnz > 0 && (!group_feat || !entry_pos)))
+    return fail(SOM_ERR_INVALID_ARG, "an output array is NULL");
+  hipError_t e = som::launch_group_plan(indptr, indices, B, F, perm, group_docs, group_offset,
+                                        group_count, group_feat, entry_pos, stream);
+  if (e != hipSuccess) return hip_fail(e, "group plan launch");
+  return ok();
+}
+
 size_t som_cluster_workspace_bytes(int64_t B, int64_t F, int64_t nnz) {
   if (B < 0 || F < 1 || nnz < 0 || B >= kI32Max) return 0;
   size_t o = 0;
-  auto take = [&](size_t bytes) { o = som::align_up(o + (bytes ? bytes : 1), 256); };
-  take(sizeof(int32_t) * F);        // df
-  take(sizeof(uint64_t) * B);       // keys
-  take(sizeof(uint64_t) * B);       // sorted keys
-  take(sizeof(int32_t) * B);        // iota
-  take(som::cluster_sort_temp_bytes(B, F));
+  take(o, sizeof(int32_t) * F);   // df
+  take(o, sizeof(uint64_t) * B);  // keys
+  take(o, sizeof(uint64_t) * B);  // sorted keys
+  take(o, sizeof(int32_t) * B);   // iota
+  take(o, som::cluster_sort_temp_bytes(B, F));
   return o;
 }
 
@@ -319,17 +424,12 @@ som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int6
   if (ws_bytes < need)
     return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
   size_t o = 0;
-  auto take = [&](size_t bytes) {
-    size_t a = o;
-    o = som::align_up(o + (bytes ? bytes : 1), 256);
-    return a;
-  };
-  const size_t o_df = take(sizeof(int32_t) * F);
-  const size_t o_keys = take(sizeof(uint64_t) * B);
-  const size_t o_sorted = take(sizeof(uint64_t) * B);
-  const size_t o_iota = take(sizeof(int32_t) * B);
+  const size_t o_df = take(o, sizeof(int32_t) * F);
+  const size_t o_keys = take(o, sizeof(uint64_t) * B);
+  const size_t o_sorted = take(o, sizeof(uint64_t) * B);
+  const size_t o_iota = take(o, sizeof(int32_t) * B);
   const size_t tb = som::cluster_sort_temp_bytes(B, F);
-  const size_t o_tmp = take(tb);
+  const size_t o_tmp = take(o, tb);
   hipError_t e = som::launch_cluster(indptr, indices, B, F, nnz, perm, at<int32_t>(ws, o_df),
                                      at<uint64_t>(ws, o_keys), at<uint64_t>(ws, o_sorted),
                                      at<int32_t>(ws, o_iota), at<void>(ws, o_tmp), tb, stream);

@@ -48,6 +48,13 @@ hipError_t launch_tile_plan(const int32_t* indptr, const int32_t* indices, int64
                             const int32_t* perm, int T, int32_t* tile_offset, int32_t* tile_count,
                             int32_t* union_feat, uint32_t* union_mask, hipStream_t stream);
 
+// Document-group plan (for the documents-on-lanes search): per group of D
+// consecutive documents of the tiled order, the sorted feature union and the
+// union position of every nonzero.
+hipError_t launch_group_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                             const int32_t* perm, int D, int32_t* group_offset, int32_t* group_count,
+                             int32_t* group_feat, int32_t* entry_pos, hipStream_t stream);
+
 struct SearchArgs {
   const float* W;
   int64_t F, N, ldw;
@@ -66,6 +73,13 @@ struct SearchArgs {
   const int32_t* union_feat;
   const uint32_t* union_mask;
   uint64_t* keys;   // [B] packed (distance, index) minima, tiled order
+  // documents-on-lanes search (kernel 2)
+  int kernel;       // 1 = neurons on lanes (tile masks), 2 = documents on lanes (groups)
+  int slice;        // kernel 2: neurons per slice (32 or 64)
+  const int32_t* group_offset;
+  const int32_t* group_count;
+  const int32_t* group_feat;
+  const int32_t* entry_pos;
   int32_t* bmu;
   float* dist;
 };

@@ -138,6 +138,70 @@ k_plan(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
   if (tid == 0) tile_count[t] = written;
 }
 
+// Document-group plan: a group is D consecutive documents of the tiled
+// order.  For each group: the sorted union of its features (group_feat, at
+// group_offset[g], group_count[g] entries) and, for every nonzero of its
+// documents, the position of that nonzero's feature inside the group's union
+// (entry_pos, indexed like `indices`).  Positions increase along a document
+// because both its features and the union are sorted.
+__global__ void __launch_bounds__(kPlanThreads)
+k_gplan(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
+        const int32_t* __restrict__ perm, int64_t B, int64_t F, int D, int window,
+        const int32_t* __restrict__ group_offset, int32_t* __restrict__ group_count,
+        int32_t* __restrict__ group_feat, int32_t* __restrict__ entry_pos) {
+  extern __shared__ uint32_t rank[];  // [window]: 0 = absent, else 1 + union position
+  __shared__ int32_t tmp[kPlanThreads];
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  constexpr int kWaves = kPlanThreads / 64;
+  const int64_t g = blockIdx.x;
+  const int64_t out0 = group_offset[g];
+  int32_t written = 0;
+  for (int64_t w0 = 0; w0 < F; w0 += window) {
+    const int wlen = static_cast<int>(F - w0 < window ? F - w0 : window);
+    for (int i = tid; i < wlen; i += kPlanThreads) rank[i] = 0u;
+    __syncthreads();
+    for (int k = wave; k < D; k += kWaves) {
+      const int64_t p = g * D + k;
+      if (p >= B) break;
+      const int64_t d = tile_doc(perm, p);
+      for (int32_t i = indptr[d] + lane; i < indptr[d + 1]; i += 64) {
+        const int64_t f = indices[i];
+        if (f >= w0 && f < w0 + wlen) rank[f - w0] = 1u;
+      }
+    }
+    __syncthreads();
+    const int per = (wlen + kPlanThreads - 1) / kPlanThreads;
+    const int a = tid * per;
+    const int b = a + per < wlen ? a + per : wlen;
+    int32_t cnt = 0;
+    for (int i = a; i < b; ++i) cnt += rank[i] != 0u;
+    int32_t total;
+    int32_t pos = block_exclusive_scan(cnt, tmp, &total);
+    for (int i = a; i < b; ++i) {
+      if (rank[i]) {
+        const int32_t at = written + pos;
+        group_feat[out0 + at] = static_cast<int32_t>(w0 + i);
+        rank[i] = static_cast<uint32_t>(at) + 1u;
+        ++pos;
+      }
+    }
+    __syncthreads();
+    for (int k = wave; k < D; k += kWaves) {
+      const int64_t p = g * D + k;
+      if (p >= B) break;
+      const int64_t d = tile_doc(perm, p);
+      for (int32_t i = indptr[d] + lane; i < indptr[d + 1]; i += 64) {
+        const int64_t f = indices[i];
+        if (f >= w0 && f < w0 + wlen) entry_pos[i] = static_cast<int32_t>(rank[f - w0]) - 1;
+      }
+    }
+    written += total;
+    __syncthreads();
+  }
+  if (tid == 0) group_count[g] = written;
+}
+
 // CSR checks: rows non-decreasing in indptr, ids in [0, F) and strictly
 // ascending within a row; optional permutation must hit every index once.
 __global__ void __launch_bounds__(256)
@@ -177,6 +241,24 @@ __global__ void k_fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
 }
 
 }  // namespace
+
+hipError_t launch_group_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
+                             const int32_t* perm, int D, int32_t* group_offset, int32_t* group_count,
+                             int32_t* group_feat, int32_t* entry_pos, hipStream_t stream) {
+  const int64_t ngroups = (B + D - 1) / D;
+  hipLaunchKernelGGL(k_tile_nnz, dim3(static_cast<uint32_t>((ngroups + 255) / 256)), dim3(256), 0,
+                     stream, indptr, perm, B, D, ngroups, group_count);
+  hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, group_count, ngroups, group_offset);
+  const int window = static_cast<int>(F < kPlanWindow ? F : kPlanWindow);
+  const size_t lds = sizeof(uint32_t) * static_cast<size_t>(window);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_gplan),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gplan, dim3(static_cast<uint32_t>(ngroups)), dim3(kPlanThreads), lds, stream,
+                     indptr, indices, perm, B, F, D, window, group_offset, group_count, group_feat,
+                     entry_pos);
+  return hipGetLastError();
+}
 
 hipError_t launch_validate(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                            int64_t nnz, const int32_t* perm, int32_t* seen, int32_t* flag,

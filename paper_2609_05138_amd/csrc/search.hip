@@ -187,6 +187,137 @@ k_search(SearchArgs a) {
   }
 }
 
+// Documents on lanes (the neuron axis cut into narrow slices).
+//
+// A workgroup of G waves owns a group of D = 64*G consecutive documents of
+// the tiled order, one document per lane, and one slice of NB neurons (32 or
+// 64: a slice's rows for all 20,000 features are 2.5-5 MB, the size of one
+// XCD's L2, so with slice-major dispatch every row is fetched from HBM about
+// once per XCD).  The group's feature union (the tile union of Section 4.1
+// with a tile of D documents) is streamed through a double-buffered LDS
+// window of kRows row slices, loaded with coalesced 128-bit loads; each lane
+// then walks its own document's features that fall in the window (their
+// union positions come from the plan, in ascending order) and adds the NB
+// weights of each into its NB accumulators.  Each document's dot product is
+// therefore summed in ascending feature order, exactly as in the
+// neurons-on-lanes kernel: results are bit-identical between the two.  The
+// lane's best neuron over the slice is folded into the document's packed key
+// with an atomic minimum, skipped when the key already holds a better value.
+template <int NB>
+struct DocsCfg {
+  static constexpr int kQ = NB / 4;              // float4 per row slice
+  static constexpr int kStride = kQ + 1;         // LDS row stride in float4 (bank spread)
+  static constexpr int kRows = NB == 32 ? 448 : 224;  // rows per window (2 windows < 160 KB)
+};
+
+template <int NB, int G>
+__global__ void __launch_bounds__(G * 64)
+k_search_docs(SearchArgs a) {
+  using C = DocsCfg<NB>;
+  constexpr int kQ = C::kQ, kStride = C::kStride, kRows = C::kRows;
+  constexpr int kThreads = G * 64;
+  constexpr int kTpr = kQ;                        // staging threads per row
+  constexpr int kRpp = kThreads / kTpr;           // rows per staging pass
+  constexpr int kPasses = (kRows + kRpp - 1) / kRpp;
+  __shared__ float4 rows[2][kRows * kStride];
+
+  const int tid = threadIdx.x;
+  const int64_t g = blockIdx.x;
+  const int64_t c = blockIdx.y;
+  const int64_t n0 = c * NB;
+  const int64_t D = static_cast<int64_t>(kThreads);
+  const int64_t p = g * D + tid;                  // this lane's document (tiled order)
+  const bool valid = p < a.B;
+  const int64_t d = valid ? (a.perm ? static_cast<int64_t>(a.perm[p]) : p) : 0;
+  const int32_t e0 = valid ? a.indptr[d] : 0;
+  const int32_t e1 = valid ? a.indptr[d + 1] : 0;
+  const int32_t cnt = a.group_count[g];
+  const int32_t goff = a.group_offset[g];
+  const int32_t nw = (cnt + kRows - 1) / kRows;
+  const int64_t ldw = a.ldw;
+
+  // staging role: row r = pass * kRpp + tid / kTpr, float4 q = tid % kTpr;
+  // columns past the row end re-read the row's last float4 (in bounds)
+  const int sq = tid % kTpr;
+  const int sr = tid / kTpr;
+  const int64_t scol = n0 + 4 * sq < ldw ? n0 + 4 * sq : ldw - 4;
+  const float* __restrict__ Wc = a.W + scol;
+  float4 stage[kPasses];
+#pragma unroll
+  for (int k = 0; k < kPasses; ++k) stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+
+  float acc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) acc[j] = 0.f;
+
+  constexpr int32_t kEnd = 0x7fffffff;
+  int32_t ptr = e0;
+  int32_t pos = ptr < e1 ? a.entry_pos[ptr] : kEnd;
+
+// staging of window w into registers, then into LDS buffer `buf`
+#define SOM_DOCS_PREFETCH(w)                                                   \
+  _Pragma("unroll") for (int k = 0; k < kPasses; ++k) {                        \
+    const int r = k * kRpp + sr;                                               \
+    const int32_t u = (w) * kRows + r;                                         \
+    const int64_t f = (r < kRows && u < cnt) ? a.group_feat[goff + u] : 0;     \
+    stage[k] = *reinterpret_cast<const float4*>(Wc + f * ldw);                 \
+  }
+#define SOM_DOCS_STORE(buf)                                                    \
+  _Pragma("unroll") for (int k = 0; k < kPasses; ++k) {                        \
+    const int r = k * kRpp + sr;                                               \
+    if (r < kRows) rows[buf][r * kStride + sq] = stage[k];                     \
+  }
+
+  if (nw > 0) {
+    SOM_DOCS_PREFETCH(0)
+    SOM_DOCS_STORE(0)
+  }
+  __syncthreads();
+  for (int32_t w = 0; w < nw; ++w) {
+    if (w + 1 < nw) { SOM_DOCS_PREFETCH(w + 1) }
+    const int32_t wbase = w * kRows;
+    const int32_t wend = wbase + kRows;
+    const float4* __restrict__ buf = rows[w & 1];
+    while (pos < wend) {
+      const int32_t nxt = ptr + 1 < e1 ? a.entry_pos[ptr + 1] : kEnd;
+      const float4* rp = buf + (pos - wbase) * kStride;
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        const float4 v = rp[q];
+        acc[4 * q + 0] += v.x;
+        acc[4 * q + 1] += v.y;
+        acc[4 * q + 2] += v.z;
+        acc[4 * q + 3] += v.w;
+      }
+      pos = nxt;
+      ++ptr;
+    }
+    if (w + 1 < nw) { SOM_DOCS_STORE((w + 1) & 1) }
+    __syncthreads();
+  }
+#undef SOM_DOCS_PREFETCH
+#undef SOM_DOCS_STORE
+
+  if (!valid) return;
+  const float nnz = static_cast<float>(e1 - e0);
+  float best = 0.f;
+  uint32_t bj = 0xffffffffu;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int64_t gj = n0 + j;
+    if (gj < a.N) {
+      const float dj = fmaf(-2.f, acc[j], nnz + a.norms[gj]);
+      if (bj == 0xffffffffu || dj < best) {  // ascending j: strict < keeps the lowest
+        best = dj;
+        bj = static_cast<uint32_t>(gj);
+      }
+    }
+  }
+  const uint64_t key = pack_key(best, bj);
+  unsigned long long* kp = reinterpret_cast<unsigned long long*>(a.keys + p);
+  if (key < *kp) atomicMin(kp, static_cast<unsigned long long>(key));
+}
+
 __global__ void __launch_bounds__(256) k_keys_init(uint64_t* __restrict__ keys, int64_t n) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < n) keys[i] = kNoKey;
@@ -224,11 +355,40 @@ hipError_t launch_tk(const SearchArgs& a, hipStream_t stream) {
   }
 }
 
+template <int NB, int G>
+hipError_t launch_docs_ng(const SearchArgs& a, hipStream_t stream) {
+  const int64_t ngroups = (a.B + 64 * G - 1) / (64 * G);
+  const dim3 grid(static_cast<uint32_t>(ngroups), static_cast<uint32_t>(a.nchunks));
+  hipLaunchKernelGGL((k_search_docs<NB, G>), grid, dim3(G * 64), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_docs(const SearchArgs& a, hipStream_t stream) {
+  if (a.slice == 32) {
+    switch (a.group) {
+      case 4: return launch_docs_ng<32, 4>(a, stream);
+      case 8: return launch_docs_ng<32, 8>(a, stream);
+      case 16: return launch_docs_ng<32, 16>(a, stream);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (a.slice == 64) {
+    switch (a.group) {
+      case 4: return launch_docs_ng<64, 4>(a, stream);
+      case 8: return launch_docs_ng<64, 8>(a, stream);
+      case 16: return launch_docs_ng<64, 16>(a, stream);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(k_keys_init, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream,
                      a.keys, a.B);
+  if (a.kernel == 2) return launch_docs(a, stream);
   switch (a.T) {
     case 1: return a.K == 4 ? launch_tk<1, 4>(a, stream) : launch_tk<1, 8>(a, stream);
     case 2: return a.K == 4 ? launch_tk<2, 4>(a, stream) : launch_tk<2, 8>(a, stream);

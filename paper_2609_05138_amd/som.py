@@ -28,9 +28,12 @@ EXPORTS = (
     "som_codebook_norms",
     "som_bmu_workspace_bytes",
     "som_bmu_search",
-    "som_tile_plan",
+    "som_plan_bytes",
+    "som_plan",
     "som_bmu_search_planned_workspace_bytes",
     "som_bmu_search_planned",
+    "som_tile_plan",
+    "som_group_plan",
     "som_cluster_workspace_bytes",
     "som_cluster_order",
 )
@@ -44,12 +47,14 @@ class SomError(RuntimeError):
 
 class som_bmu_opts(ctypes.Structure):
     _fields_ = [
+        ("kernel", ctypes.c_int32),
         ("tile_docs", ctypes.c_int32),
         ("lane_neurons", ctypes.c_int32),
         ("group_tiles", ctypes.c_int32),
         ("mask_mode", ctypes.c_int32),
+        ("slice_neurons", ctypes.c_int32),
         ("validate", ctypes.c_int32),
-        ("reserved", ctypes.c_int32 * 3),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -82,13 +87,19 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.som_bmu_search.restype = _i32
     lib.som_bmu_search.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp,
                                    ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
-    lib.som_tile_plan.restype = _i32
-    lib.som_tile_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp]
+    lib.som_plan_bytes.restype = _sz
+    lib.som_plan_bytes.argtypes = [_i64, _i64, ctypes.POINTER(som_bmu_opts)]
+    lib.som_plan.restype = _i32
+    lib.som_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
     lib.som_bmu_search_planned_workspace_bytes.restype = _sz
     lib.som_bmu_search_planned_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(som_bmu_opts)]
     lib.som_bmu_search_planned.restype = _i32
-    lib.som_bmu_search_planned.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+    lib.som_bmu_search_planned.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _i64, _i64, _vp, _vp, _sz,
                                            _vp, _vp, ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
+    lib.som_tile_plan.restype = _i32
+    lib.som_tile_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp]
+    lib.som_group_plan.restype = _i32
+    lib.som_group_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp]
     lib.som_cluster_workspace_bytes.restype = _sz
     lib.som_cluster_workspace_bytes.argtypes = [_i64, _i64, _i64]
     lib.som_cluster_order.restype = _i32
@@ -123,9 +134,10 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _opts(tile_docs=0, lane_neurons=0, group_tiles=0, mask_mode=0, validate=False) -> som_bmu_opts:
-    return som_bmu_opts(int(tile_docs), int(lane_neurons), int(group_tiles), int(mask_mode),
-                        int(bool(validate)))
+def _opts(kernel=0, tile_docs=0, lane_neurons=0, group_tiles=0, mask_mode=0, slice_neurons=0,
+          validate=False) -> som_bmu_opts:
+    return som_bmu_opts(int(kernel), int(tile_docs), int(lane_neurons), int(group_tiles), int(mask_mode),
+                        int(slice_neurons), int(bool(validate)), 0)
 
 
 def _workspace(nbytes: int, device) -> torch.Tensor:
@@ -168,8 +180,8 @@ def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, i
                    ws: Optional[torch.Tensor] = None, stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
     """BMU index (int32) and squared distance (fp32) of every CSR document.
 
-    ``knobs``: tile_docs, lane_neurons, group_tiles, mask_mode (fields of
-    som_bmu_opts; none changes a result)."""
+    ``knobs``: kernel, tile_docs, lane_neurons, group_tiles, mask_mode,
+    slice_neurons (fields of som_bmu_opts; none changes a result)."""
     lib = load()
     _dev(W, torch.float32, "W")
     _dev(norms, torch.float32, "norms")
@@ -202,22 +214,75 @@ def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, i
     return bmu, dist
 
 
-class TilePlan:
-    """Device arrays of a tile plan (see som_tile_plan) and how it was built."""
+class Plan:
+    """An opaque search plan (device buffer) and how it was built."""
 
-    def __init__(self, tile_offset, tile_count, union_feat, union_mask, tile_docs, B, perm):
-        self.tile_offset = tile_offset
-        self.tile_count = tile_count
-        self.union_feat = union_feat
-        self.union_mask = union_mask
-        self.tile_docs = tile_docs
+    def __init__(self, buf, knobs, B, nnz, perm):
+        self.buf = buf
+        self.knobs = dict(knobs)
         self.B = B
+        self.nnz = nnz
         self.perm = perm
 
 
+def som_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, perm: Optional[torch.Tensor] = None,
+             plan: Optional[torch.Tensor] = None, stream=None, **knobs) -> Plan:
+    """Plan of a batch for som_bmu_search_planned (codebook-independent)."""
+    lib = load()
+    _dev(indptr, torch.int32, "indptr")
+    _dev(indices, torch.int32, "indices")
+    B = indptr.numel() - 1
+    nnz = indices.numel()
+    if perm is not None:
+        _dev(perm, torch.int32, "perm")
+    o = _opts(**knobs)
+    need = int(lib.som_plan_bytes(B, nnz, ctypes.byref(o)))
+    if plan is None:
+        plan = _workspace(need, indptr.device)
+    _dev(plan, torch.uint8, "plan")
+    _check(lib.som_plan(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), ctypes.byref(o), _ptr(plan),
+                        plan.numel(), _stream(stream)))
+    return Plan(plan, knobs, B, nnz, perm)
+
+
+def som_bmu_search_planned_workspace_bytes(N: int, B: int, **knobs) -> int:
+    o = _opts(**knobs)
+    return int(load().som_bmu_search_planned_workspace_bytes(N, B, ctypes.byref(o)))
+
+
+def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, plan: Plan,
+                           N: Optional[int] = None, bmu: Optional[torch.Tensor] = None,
+                           dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                           stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """The search stage on a prebuilt plan (same indptr, perm and knobs)."""
+    lib = load()
+    _dev(W, torch.float32, "W")
+    _dev(norms, torch.float32, "norms")
+    _dev(indptr, torch.int32, "indptr")
+    F, ldw = W.shape
+    n = ldw if N is None else int(N)
+    B = indptr.numel() - 1
+    if B != plan.B:
+        raise ValueError("plan was built for another batch")
+    if bmu is None:
+        bmu = torch.empty(B, dtype=torch.int32, device=W.device)
+    if dist is None:
+        dist = torch.empty(B, dtype=torch.float32, device=W.device)
+    _dev(bmu, torch.int32, "bmu")
+    _dev(dist, torch.float32, "dist")
+    o = _opts(**plan.knobs)
+    if ws is None:
+        ws = _workspace(lib.som_bmu_search_planned_workspace_bytes(n, B, ctypes.byref(o)), W.device)
+    _dev(ws, torch.uint8, "ws")
+    _check(lib.som_bmu_search_planned(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), B, plan.nnz,
+                                      _ptr(plan.perm), _ptr(plan.buf), plan.buf.numel(), _ptr(bmu),
+                                      _ptr(dist), ctypes.byref(o), _ptr(ws), ws.numel(), _stream(stream)))
+    return bmu, dist
+
+
 def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs: int = 8,
-                  perm: Optional[torch.Tensor] = None, stream=None) -> TilePlan:
-    """Per-tile feature unions and membership masks of the tiled order."""
+                  perm: Optional[torch.Tensor] = None, stream=None):
+    """Kernel-1 tile plan as explicit arrays: (tile_offset, tile_count, union_feat, union_mask)."""
     lib = load()
     _dev(indptr, torch.int32, "indptr")
     _dev(indices, torch.int32, "indices")
@@ -234,46 +299,29 @@ def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs
     union_mask = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
     _check(lib.som_tile_plan(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), T, _ptr(tile_offset),
                              _ptr(tile_count), _ptr(union_feat), _ptr(union_mask), _stream(stream)))
-    return TilePlan(tile_offset, tile_count[:ntiles], union_feat, union_mask, T, B, perm)
+    return tile_offset, tile_count[:ntiles], union_feat, union_mask
 
 
-def som_bmu_search_planned_workspace_bytes(N: int, B: int, **knobs) -> int:
-    o = _opts(**knobs)
-    return int(load().som_bmu_search_planned_workspace_bytes(N, B, ctypes.byref(o)))
-
-
-def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, plan: TilePlan,
-                           N: Optional[int] = None, bmu: Optional[torch.Tensor] = None,
-                           dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                           stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
-    """The search stage on a prebuilt plan (same indptr and perm)."""
+def som_group_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, group_docs: int = 1024,
+                   perm: Optional[torch.Tensor] = None, stream=None):
+    """Kernel-2 group plan as explicit arrays: (group_offset, group_count, group_feat, entry_pos)."""
     lib = load()
-    _dev(W, torch.float32, "W")
-    _dev(norms, torch.float32, "norms")
     _dev(indptr, torch.int32, "indptr")
-    F, ldw = W.shape
-    n = ldw if N is None else int(N)
+    _dev(indices, torch.int32, "indices")
     B = indptr.numel() - 1
-    if B != plan.B:
-        raise ValueError("plan was built for another batch")
-    if bmu is None:
-        bmu = torch.empty(B, dtype=torch.int32, device=W.device)
-    if dist is None:
-        dist = torch.empty(B, dtype=torch.float32, device=W.device)
-    _dev(bmu, torch.int32, "bmu")
-    _dev(dist, torch.float32, "dist")
-    knobs = dict(knobs)
-    if knobs.setdefault("tile_docs", plan.tile_docs) != plan.tile_docs:
-        raise ValueError("tile_docs differs from the plan's")
-    o = _opts(**knobs)
-    if ws is None:
-        ws = _workspace(lib.som_bmu_search_planned_workspace_bytes(n, B, ctypes.byref(o)), W.device)
-    _dev(ws, torch.uint8, "ws")
-    _check(lib.som_bmu_search_planned(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), B, _ptr(plan.perm),
-                                      _ptr(plan.tile_offset), _ptr(plan.tile_count), _ptr(plan.union_feat),
-                                      _ptr(plan.union_mask), _ptr(bmu), _ptr(dist), ctypes.byref(o),
-                                      _ptr(ws), ws.numel(), _stream(stream)))
-    return bmu, dist
+    nnz = indices.numel()
+    D = int(group_docs)
+    ng = (B + D - 1) // D if D > 0 else 0
+    dev = indptr.device
+    if perm is not None:
+        _dev(perm, torch.int32, "perm")
+    offset = torch.empty(ng + 1, dtype=torch.int32, device=dev)
+    count = torch.empty(max(ng, 1), dtype=torch.int32, device=dev)
+    feat = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    pos = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    _check(lib.som_group_plan(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), D, _ptr(offset),
+                              _ptr(count), _ptr(feat), _ptr(pos), _stream(stream)))
+    return offset, count[:ng], feat, pos
 
 
 def som_cluster_workspace_bytes(B: int, F: int, nnz: int) -> int:

@@ -42,18 +42,22 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 3
+    assert som.som_abi_version() == 4
 
 
 def test_workspace_sizes_are_host_only(lib):
-    o = som.som_bmu_opts()
-    a = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o))
-    assert a > 0 and a % 256 == 0
-    # the plan (two int32 per nonzero) dominates; one packed key per document
-    assert a >= 8 * 84_000_000 + 8 * (1 << 20)
-    o8 = som.som_bmu_opts(16, 8, 4, 0, 1)
-    b = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o8))
-    assert b > a                   # validation needs a scratch array
+    for kernel in (0, 1, 2):
+        o = som.som_bmu_opts(kernel)
+        a = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o))
+        assert a > 0 and a % 256 == 0
+        # the plan (two int32 per nonzero) dominates; one packed key per document
+        assert a >= 8 * 84_000_000 + 8 * (1 << 20)
+        assert lib.som_plan_bytes(1 << 20, 84_000_000, ctypes.byref(o)) >= 8 * 84_000_000
+        assert lib.som_bmu_search_planned_workspace_bytes(262144, 1 << 20, ctypes.byref(o)) >= 8 * (1 << 20)
+        v = som.som_bmu_opts(kernel)
+        v.validate = 1
+        b = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(v))
+        assert b > a                   # validation needs a scratch array
     assert lib.som_bmu_workspace_bytes(0, 10, 10, 10, None) == 0
     assert lib.som_bmu_workspace_bytes(10, 10, -1, 10, None) == 0
     bad = som.som_bmu_opts(3)
@@ -106,10 +110,11 @@ def test_search_rejects_bad_arguments(lib):
     assert call(ws=null)[0] == som.SOM_ERR_WORKSPACE
     assert call(ws=ws_bad)[0] == som.SOM_ERR_INVALID_ARG
     res = som.som_bmu_opts()
-    res.reserved[1] = 1
-    for bad in (som.som_bmu_opts(3), som.som_bmu_opts(0, 5), som.som_bmu_opts(0, 0, 3), res,
-                som.som_bmu_opts(0, 0, 16), som.som_bmu_opts(0, 0, 0, 3), som.som_bmu_opts(32, 8),
-                som.som_bmu_opts(0, 0, 0, 0, 2), som.som_bmu_opts(0, 0, 0, -1)):
+    res.reserved = 1
+    O = som.som_bmu_opts
+    for bad in (O(3), O(1, 5), O(1, 0, 3), res, O(1, 0, 0, 16), O(1, 0, 0, 0, 3), O(1, 32, 8),
+                O(0, 0, 0, 0, 0, 0, 2), O(1, 0, 0, -1), O(2, 8), O(2, 0, 4), O(2, 0, 0, 1),
+                O(2, 0, 0, 0, 1), O(2, 0, 0, 0, 0, 48), O(1, 0, 0, 0, 0, 32)):
         st, msg = call(opts=ctypes.byref(bad))
         assert st == som.SOM_ERR_INVALID_ARG, msg
     # an empty batch is a valid no-op that touches nothing
@@ -126,18 +131,28 @@ def test_plan_and_cluster_reject_bad_arguments(lib):
     assert st == som.SOM_ERR_INVALID_ARG
     st, _ = _status(lib, "som_tile_plan", fake, fake, 4, 8, 10, null, 4, null, fake, fake, fake, null)
     assert st == som.SOM_ERR_INVALID_ARG
-    o = som.som_bmu_opts(4)
+    st, msg = _status(lib, "som_group_plan", fake, fake, 4, 8, 10, null, 0, fake, fake, fake, fake, null)
+    assert st == som.SOM_ERR_INVALID_ARG and "group_docs" in msg
+    o = som.som_bmu_opts()
     assert lib.som_bmu_search_planned_workspace_bytes(1024, 100, ctypes.byref(o)) >= 8 * 100
-    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, fake, fake, fake,
-                    fake, fake, fake, ctypes.byref(o), fake, 4, null)
+    big = 1 << 30
+    # W, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist, opts, ws, ws_bytes, stream
+    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, 10, null, fake, big,
+                    fake, fake, ctypes.byref(o), fake, 4, null)
     assert st == som.SOM_ERR_WORKSPACE
-    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, null, fake, fake,
-                    fake, fake, fake, ctypes.byref(o), fake, 1 << 20, null)
+    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, 10, null, null, big,
+                    fake, fake, ctypes.byref(o), fake, big, null)
     assert st == som.SOM_ERR_INVALID_ARG
-    v = som.som_bmu_opts(4, 0, 0, 0, 1)
-    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, null, fake, fake, fake,
-                    fake, fake, fake, ctypes.byref(v), fake, 1 << 20, null)
+    st, msg = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, 10, null, fake, 16,
+                      fake, fake, ctypes.byref(o), fake, big, null)
+    assert st == som.SOM_ERR_INVALID_ARG and "plan" in msg
+    v = som.som_bmu_opts()
+    v.validate = 1
+    st, _ = _status(lib, "som_bmu_search_planned", fake, 8, 8, 8, fake, fake, 4, 10, null, fake, big,
+                    fake, fake, ctypes.byref(v), fake, big, null)
     assert st == som.SOM_ERR_INVALID_ARG
+    st, _ = _status(lib, "som_plan", fake, fake, 4, 8, 10, null, ctypes.byref(o), fake, 16, null)
+    assert st == som.SOM_ERR_WORKSPACE
     st, _ = _status(lib, "som_cluster_order", fake, fake, 4, 8, 10, null, fake, 1 << 20, null)
     assert st == som.SOM_ERR_INVALID_ARG
     st, _ = _status(lib, "som_cluster_order", fake, fake, 4, 8, 10, fake, null, 1 << 20, null)

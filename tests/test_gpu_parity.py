@@ -106,8 +106,9 @@ def test_norms_dyadic_bit_exact():
 # exact cases: hand-worked examples and dyadic codebooks
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("T", TILES)
-def test_hand_examples_bit_exact(T):
+@pytest.mark.parametrize("knobs", [dict(kernel=1, tile_docs=T) for T in TILES]
+                         + [dict(kernel=2, group_tiles=G, slice_neurons=NB) for G in (4, 16) for NB in (32, 64)])
+def test_hand_examples_bit_exact(knobs):
     ex_all = json.load(open(os.path.join(GOLDEN, "hand_examples.json")))["examples"]
     for ex in ex_all:
         F, N = ex["F"], ex["N"]
@@ -117,7 +118,7 @@ def test_hand_examples_bit_exact(T):
                 W[f, j] = float(Fraction(v))
         docs = [d["features"] for d in ex["docs"]]
         indptr, indices = _csr(docs)
-        bmu, dist, norms = _search(W, indptr, indices, tile_docs=T)
+        bmu, dist, norms = _search(W, indptr, indices, **knobs)
         assert norms.tolist() == [float(Fraction(v)) for v in ex["norms"]]
         assert bmu.tolist() == [d["bmu"] for d in ex["docs"]]
         assert dist.tolist() == [float(Fraction(d["d"][d["bmu"]])) for d in ex["docs"]]
@@ -137,8 +138,9 @@ def test_dyadic_codebook_bit_exact_with_ties(N):
     docs = _random_docs(rng, B, F, mean=12, empty_every=17, big_every=50, big=60)
     indptr, indices = _csr(docs)
     exact = oracle.bmu_search_exact(K, 2, indptr, indices)
-    for T in (1, 8, 32):
-        bmu, dist, _ = _search(W, indptr, indices, tile_docs=T)
+    for knobs in (dict(kernel=1, tile_docs=1), dict(kernel=1, tile_docs=8), dict(kernel=1, tile_docs=32),
+                  dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64)):
+        bmu, dist, _ = _search(W, indptr, indices, **knobs)
         assert bmu.tolist() == [e[2][0] for e in exact]
         assert [Fraction(float(x)) for x in dist] == [Fraction(e[1], 16) for e in exact]
 
@@ -155,7 +157,7 @@ def test_tile_plan_bit_exact(T):
     for perm in (None, rng.permutation(1001)):
         pl = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), 2048, T,
                                perm=None if perm is None else _dev_i32(perm))
-        off, cnt, uf, um = (x.cpu().numpy() for x in (pl.tile_offset, pl.tile_count, pl.union_feat, pl.union_mask))
+        off, cnt, uf, um = (x.cpu().numpy() for x in pl)
         tiles = oracle.tile_union(indptr, indices, T, perm)
         assert len(cnt) == len(tiles)
         order = np.arange(1001) if perm is None else perm
@@ -173,10 +175,33 @@ def test_tile_plan_large_feature_ids_use_several_windows():
     docs = _random_docs(rng, 130, F, mean=30, empty_every=9)
     indptr, indices = _csr(docs)
     pl = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), F, 4)
-    off, cnt, uf, um = (x.cpu().numpy() for x in (pl.tile_offset, pl.tile_count, pl.union_feat, pl.union_mask))
+    off, cnt, uf, um = (x.cpu().numpy() for x in pl)
     for t, (feats, masks) in enumerate(oracle.tile_union(indptr, indices, 4)):
         assert uf[off[t]:off[t] + cnt[t]].tolist() == feats.tolist()
         assert um[off[t]:off[t] + cnt[t]].view(np.uint32).tolist() == masks.astype(np.uint32).tolist()
+
+
+@pytest.mark.parametrize("D", [1, 7, 256, 1024])
+def test_group_plan_bit_exact(D):
+    """Group union = tile union with a tile of D documents; entry_pos = the
+    position of each nonzero's feature in its group's union."""
+    from synth import documents
+    indptr, indices = documents(1, 0, n_docs=2500)
+    B = 2500
+    rng = np.random.default_rng(D)
+    for perm in (None, rng.permutation(B)):
+        off, cnt, gf, pos = (x.cpu().numpy() for x in som.som_group_plan(
+            _dev_i32(indptr), _dev_i32(indices), 2048, D, perm=None if perm is None else _dev_i32(perm)))
+        order = np.arange(B) if perm is None else perm
+        groups = oracle.tile_union(indptr, indices, D, perm)
+        assert len(cnt) == len(groups)
+        for g, (feats, _) in enumerate(groups):
+            assert cnt[g] == len(feats)
+            assert gf[off[g]:off[g] + cnt[g]].tolist() == feats.tolist()
+            rank = {int(f): i for i, f in enumerate(feats)}
+            for d in order[g * D:(g + 1) * D]:
+                a, b = indptr[d], indptr[d + 1]
+                assert pos[a:b].tolist() == [rank[int(f)] for f in indices[a:b]]
 
 
 def test_cluster_order_golden():
@@ -214,8 +239,9 @@ def test_config1_every_document():
     from synth import codebook, documents
     W = codebook(1)
     indptr, indices = documents(1, 0)
-    for T in (1, 4, 8, 32):
-        bmu, dist, _ = _search(W, indptr, indices, tile_docs=T)
+    for knobs in (dict(kernel=1, tile_docs=1), dict(kernel=1, tile_docs=8), dict(kernel=2),
+                  dict(kernel=2, group_tiles=4, slice_neurons=64)):
+        bmu, dist, _ = _search(W, indptr, indices, **knobs)
         W64 = W.astype(np.float64)
         _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, bmu, dist, range(len(indptr) - 1))
 
@@ -248,14 +274,16 @@ def test_results_identical_across_tile_chunk_and_order():
     ref = None
     rng = np.random.default_rng(5)
     perms = [None, rng.permutation(3000), oracle.cluster_order(indptr, indices, 20000)]
+    variants = [dict(kernel=2, group_tiles=G, slice_neurons=NB) for G in (4, 8, 16) for NB in (32, 64)]
     for T in TILES:
         for K, G, mode in ((0, 0, 0), (4, 1, 1), (8 if T < 32 else 4, 8, 2), (4, 2, 2)):
-            for perm in perms[:2] if T != 8 else perms:
-                out = _search(W, indptr, indices, perm=perm, tile_docs=T, lane_neurons=K, group_tiles=G,
-                              mask_mode=mode)
-                if ref is None:
-                    ref = out
-                assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (T, K, G, mode)
+            variants.append(dict(kernel=1, tile_docs=T, lane_neurons=K, group_tiles=G, mask_mode=mode))
+    for i, v in enumerate(variants):
+        for perm in perms if i % 5 == 0 else perms[:2]:
+            out = _search(W, indptr, indices, perm=perm, **v)
+            if ref is None:
+                ref = out
+            assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), v
 
 
 def test_repeated_runs_are_bit_identical():
@@ -323,13 +351,17 @@ def test_planned_search_reuses_a_plan_across_codebooks():
     indptr, indices = documents(1, 0, n_docs=2500)
     ip, ix = _dev_i32(indptr), _dev_i32(indices)
     perm = _dev_i32(oracle.cluster_order(indptr, indices, 2048))
-    plan = som.som_tile_plan(ip, ix, 2048, 4, perm=perm)
+    plan = som.som_plan(ip, ix, 2048, perm=perm)
+    plan1 = som.som_plan(ip, ix, 2048, perm=perm, kernel=1, tile_docs=4)
     for seed in (0, 1):
         W = codebook(1, seed=seed)
         Wd, _ = _dev_W(W)
         norms = som.som_codebook_norms(Wd)
         a = som.som_bmu_search_planned(Wd, norms, ip, plan)
-        b = som.som_bmu_search(Wd, norms, ip, ix, perm=perm, tile_docs=4)
+        b = som.som_bmu_search(Wd, norms, ip, ix, perm=perm, kernel=1, tile_docs=4)
+        c = som.som_bmu_search_planned(Wd, norms, ip, plan1)
+        torch.cuda.synchronize()
+        assert torch.equal(a[0], c[0]) and torch.equal(a[1], c[1])
         torch.cuda.synchronize()
         assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
         W64 = W.astype(np.float64)
