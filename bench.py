@@ -4,9 +4,10 @@
 One step = one pass of the whole path over one CSR batch resident in HBM:
 codebook norms, tile-membership clustering, tile plan, fused tiled search
 with the chunk merge.  Default workload: the 512x512 map (N = 262,144
-neurons, F = 20,000 features, fp32 feature-major codebook, 21 GB) against
-the first 1,048,576-document batch of the 2,000,000-document Poisson(80),
-Zipf(1.1) pass.  Prints one JSON line (rank 0).
+neurons, F = 20,000 features, fp32 feature-major codebook, 21 GB, rows at the
+library's recommended stride) against the first 1,048,576-document batch of
+the 2,000,000-document Poisson(80), Zipf(1.1) pass.  Prints one JSON line
+(rank 0).
 """
 
 from __future__ import annotations
@@ -39,6 +40,7 @@ def parse():
     p.add_argument("--config", type=int, default=4, help="workload (1..5)")
     p.add_argument("--batch", type=int, default=0)
     p.add_argument("--docs", type=int, default=0, help="override documents per batch (0 = config)")
+    p.add_argument("--ldw", type=int, default=0, help="codebook row stride in floats (0 = recommended)")
     p.add_argument("--kernel", type=int, default=0, help="0 auto, 1 neurons on lanes, 2 documents on lanes")
     p.add_argument("--tile-docs", type=int, default=0)
     p.add_argument("--lane-neurons", type=int, default=0)
@@ -93,7 +95,15 @@ def main():
     nnz = int(indices.size)
     log(args, f"{B} documents, nnz={nnz} generated in {time.time() - t:.1f}s")
 
-    Wd = torch.from_numpy(W).to(dev)
+    ldw = args.ldw or som.som_codebook_ldw(N)
+    if ldw < N:
+        raise SystemExit(f"--ldw must be >= N = {N}")
+    Wd = torch.empty((F, ldw), dtype=torch.float32, device=dev)
+    Wh = torch.from_numpy(W)
+    for r0 in range(0, F, 1024):
+        Wd[r0:r0 + 1024, :N].copy_(Wh[r0:r0 + 1024].to(dev))
+    if ldw > N:
+        Wd[:, N:].zero_()
     ip = torch.from_numpy(indptr).to(dev)
     ix = torch.from_numpy(indices).to(dev)
     norms = torch.empty(N, dtype=torch.float32, device=dev)
@@ -102,7 +112,7 @@ def main():
     perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
     knobs = dict(kernel=args.kernel, tile_docs=args.tile_docs, lane_neurons=args.lane_neurons,
                  group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons)
-    kernel = args.kernel or 2
+    kernel = args.kernel or 1
     # documents that share one sweep of a union: a kernel-1 tile or a kernel-2 group
     T = (args.tile_docs or 8) if kernel == 1 else 64 * (args.group_tiles or 16)
     cl_ws = torch.empty(max(som.som_cluster_workspace_bytes(B, F, nnz), 1), dtype=torch.uint8, device=dev)
@@ -154,7 +164,7 @@ def main():
     else:
         cnt = som.som_group_plan(ip, ix, F, T, perm=perm)[1]
     union_total = int(cnt.to(torch.int64).sum().item())
-    measured = MEASURED_TRAFFIC.get((cfg.name, args.batch, B, kernel, json.dumps(knobs, sort_keys=True)))
+    measured = MEASURED_TRAFFIC.get((cfg.name, args.batch, B, ldw, kernel, json.dumps(knobs, sort_keys=True)))
     pairs = B * N
     value = pairs / (ms_step * 1e-3)
     search_s = st[3] * 1e-3
@@ -212,7 +222,7 @@ def main():
         "config": {
             "workload": (f"{cfg.name}: map {int(round(N ** 0.5))}^2 (N={N}), F={F}, fp32 feature-major codebook; "
                          f"batch {args.batch}: {B} binary documents, nnz={nnz}"),
-            "N": N, "F": F, "B": B, "nnz": nnz, "docs_per_union_sweep": T,
+            "N": N, "F": F, "ldw": ldw, "B": B, "nnz": nnz, "docs_per_union_sweep": T,
             "knobs": {k: (v or "auto") for k, v in knobs.items()}, "clustered": perm is not None,
             "bmu_pass_ms": float(st[1] + st[2] + st[3]),
         },

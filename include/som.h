@@ -68,9 +68,9 @@ typedef enum som_status {
  * Either way the neuron axis is cut into slices whose minima are merged
  * (Section 4.2) and the argmin is fused (Section 3). */
 typedef struct som_bmu_opts {
-  int32_t kernel;        /* 0 = auto, 1 = neurons on lanes, 2 = documents on lanes */
-  int32_t tile_docs;     /* kernel 1: T = 0 (auto), 1, 2, 4, 8, 16 or 32 */
-  int32_t lane_neurons;  /* kernel 1: K = 0 (auto), 4 or 8; T = 32 needs 4 */
+  int32_t kernel;        /* 0 = auto (kernel 1), 1 = neurons on lanes, 2 = documents on lanes */
+  int32_t tile_docs;     /* kernel 1: T = 0 (auto: 8), 1, 2, 4, 8, 16 or 32 */
+  int32_t lane_neurons;  /* kernel 1: K = 0 (auto: 4), 4 or 8; T = 32 needs 4 */
   int32_t group_tiles;   /* kernel 1: tiles per workgroup, 0 (auto), 1, 2, 4 or 8;
                             kernel 2: waves per workgroup G, 0 (auto), 4, 8 or 16 */
   int32_t mask_mode;     /* kernel 1: 0 = auto, 1 = branch-free multiply by the membership
@@ -94,6 +94,18 @@ const char* som_last_error(void);
  * Errors: SOM_ERR_INVALID_ARG for F < 1, N < 1, bad ldw/alignment or NULL. */
 som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
                               hipStream_t stream);
+
+/* Recommended row stride ldw (in floats) of a feature-major codebook of N
+ * neurons; host-only, enqueues nothing.  The search reads each feature row
+ * in 1 KB slices (256 neurons), the same slice of every row at once.  The L2
+ * of each XCD interleaves its 16 channels on 128-byte lines, so with a row
+ * stride that is a multiple of 2 KB every row's slice falls on the same 8
+ * channels and only half of the L2 holds the slice.  The recommended stride
+ * is N rounded up to a multiple of 64 floats (256-byte aligned rows), plus
+ * 64 floats when that is a multiple of 512, which rotates consecutive rows
+ * across all channels.  Any ldw >= N with ldw % 4 == 0 stays valid; this is
+ * a layout choice for speed only.  Returns 0 for N < 1. */
+int64_t som_codebook_ldw(int64_t N);
 
 /* Bytes of device workspace som_bmu_search needs for these sizes and
  * options (0 if the arguments are invalid). */

@@ -19,6 +19,7 @@ from .som import (  # noqa: F401
     som_plan,
     som_cluster_order,
     som_cluster_workspace_bytes,
+    som_codebook_ldw,
     som_codebook_norms,
     som_last_error,
     som_tile_plan,

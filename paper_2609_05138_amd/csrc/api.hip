@@ -60,10 +60,10 @@ som_status check_batch(const int32_t* indptr, const int32_t* indices, int64_t B,
 // Resolved knobs.  Defaults chosen by measurement on MI355X (512^2 map,
 // F = 20,000, 1M-document batches).
 struct Plan {
-  int kernel = 2;
+  int kernel = 1;
   // kernel 1
   int T = 8;
-  int K = 8;
+  int K = 4;
   int mask_mode = 1;  // SearchArgs encoding: 0 = fma, 1 = branch
   // kernel 1: tiles per workgroup; kernel 2: waves per workgroup
   int group = 16;
@@ -80,13 +80,13 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
   if (o.reserved != 0) return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
   if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
   if (o.kernel < 0 || o.kernel > 2) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1 or 2");
-  const int kernel = o.kernel ? o.kernel : 2;
+  const int kernel = o.kernel ? o.kernel : 1;
   p->kernel = kernel;
   if (kernel == 1) {
     const int T = o.tile_docs ? o.tile_docs : 8;
     if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
       return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 1, 2, 4, 8, 16 or 32");
-    const int K = o.lane_neurons ? o.lane_neurons : (T >= 32 ? 4 : 8);
+    const int K = o.lane_neurons ? o.lane_neurons : 4;
     if (K != 4 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0, 4 or 8");
     if (T == 32 && K != 4) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 4 when tile_docs is 32");
     const int G = o.group_tiles ? o.group_tiles : 1;
@@ -244,9 +244,16 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 4; }
+int32_t som_abi_version(void) { return 5; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
+
+int64_t som_codebook_ldw(int64_t N) {
+  if (N < 1) return 0;
+  int64_t ldw = (N + 63) / 64 * 64;
+  if (ldw % 512 == 0) ldw += 64;
+  return ldw;
+}
 
 som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
                               hipStream_t stream) {

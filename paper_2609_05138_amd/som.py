@@ -26,6 +26,7 @@ EXPORTS = (
     "som_abi_version",
     "som_last_error",
     "som_codebook_norms",
+    "som_codebook_ldw",
     "som_bmu_workspace_bytes",
     "som_bmu_search",
     "som_plan_bytes",
@@ -82,6 +83,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.som_last_error.argtypes = []
     lib.som_codebook_norms.restype = _i32
     lib.som_codebook_norms.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp]
+    lib.som_codebook_ldw.restype = _i64
+    lib.som_codebook_ldw.argtypes = [_i64]
     lib.som_bmu_workspace_bytes.restype = _sz
     lib.som_bmu_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, ctypes.POINTER(som_bmu_opts)]
     lib.som_bmu_search.restype = _i32
@@ -151,6 +154,11 @@ def som_abi_version() -> int:
 
 def som_last_error() -> str:
     return load().som_last_error().decode(errors="replace")
+
+
+def som_codebook_ldw(N: int) -> int:
+    """Recommended row stride (floats) of a feature-major codebook of N neurons."""
+    return int(load().som_codebook_ldw(int(N)))
 
 
 def som_codebook_norms(W: torch.Tensor, N: Optional[int] = None, norms: Optional[torch.Tensor] = None,

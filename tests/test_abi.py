@@ -42,7 +42,18 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 4
+    assert som.som_abi_version() == 5
+
+
+def test_codebook_ldw_is_host_only(lib):
+    # the recommended stride is 256-byte aligned, never below N, and never a
+    # multiple of 2 KB (so row slices rotate over the L2 channels)
+    for N, want in ((262144, 262208), (65536, 65600), (16384, 16448), (1024, 1088), (512, 576),
+                    (3, 64), (64, 64), (100, 128), (1000, 1088), (1100, 1152), (1 << 30, (1 << 30) + 64)):
+        got = som.som_codebook_ldw(N)
+        assert got == want, (N, got)
+        assert got >= N and got % 64 == 0 and (4 * got) % 2048 != 0
+    assert som.som_codebook_ldw(0) == 0 and som.som_codebook_ldw(-5) == 0
 
 
 def test_workspace_sizes_are_host_only(lib):

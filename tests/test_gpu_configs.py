@@ -3,7 +3,8 @@
 For the 256^2 and 512^2 maps (N = 65,536 and 262,144 neurons, F = 20,000,
 codebooks of 5.2 and 21 GB) the oracle cannot score a whole batch, so each
 test runs the device search on a full batch in the launch configuration the
-benchmark uses and checks:
+benchmark uses (default knobs, codebook rows at the recommended stride) and
+checks:
   * a seeded sample of documents (always including the first and the last)
     against the fp64 oracle under the acceptance rule, and
   * every document's reported distance against the fp64 distance of the
@@ -36,12 +37,16 @@ def _run(cfg_key, batch, cluster, sample, seed):
     indptr, indices = documents(cfg, batch)
     B = len(indptr) - 1
     print(f"[cfg{cfg_key} batch {batch}] B={B} nnz={len(indices)} N={cfg.N}", flush=True)
-    Wd = torch.from_numpy(W).to(dev)
+    ldw = som.som_codebook_ldw(cfg.N)
+    Wd = torch.zeros((cfg.F, ldw), dtype=torch.float32, device=dev)
+    Wh = torch.from_numpy(W)
+    for r0 in range(0, cfg.F, 1024):
+        Wd[r0:r0 + 1024, :cfg.N].copy_(Wh[r0:r0 + 1024].to(dev))
     ip = torch.from_numpy(indptr).to(dev)
     ix = torch.from_numpy(indices).to(dev)
-    norms = som.som_codebook_norms(Wd)
+    norms = som.som_codebook_norms(Wd, N=cfg.N)
     perm = som.som_cluster_order(ip, ix, cfg.F) if cluster else None
-    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, perm=perm)
+    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm)
     torch.cuda.synchronize()
     bmu, dist = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
     if perm is not None:

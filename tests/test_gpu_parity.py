@@ -251,7 +251,7 @@ def test_config2_first_batch():
     W = codebook(2)
     indptr, indices = documents(2, 0)                   # 65,536 documents
     B = len(indptr) - 1
-    bmu, dist, _ = _search(W, indptr, indices)
+    bmu, dist, _ = _search(W, indptr, indices, ldw=som.som_codebook_ldw(W.shape[1]))
     W64 = W.astype(np.float64)
     norms64 = oracle.codebook_norms(W64)
     rng = np.random.default_rng(0)
@@ -284,6 +284,11 @@ def test_results_identical_across_tile_chunk_and_order():
             if ref is None:
                 ref = out
             assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), v
+    # the row stride is a layout choice only
+    for ldw in (som.som_codebook_ldw(4100), 4104, 4100 + 1024):
+        for v in (dict(), dict(kernel=1, lane_neurons=8), dict(kernel=2)):
+            out = _search(W, indptr, indices, ldw=ldw, **v)
+            assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (ldw, v)
 
 
 def test_repeated_runs_are_bit_identical():
