@@ -29,7 +29,13 @@ HBM_PEAK_BPS = 8.0e12
 # default search configuration on the default workload: FETCH_SIZE x 2.0 +
 # WRITE_SIZE x 1.0 (scales from a 4 GiB copy).  Reported only when this run
 # matches that configuration; any kernel change invalidates it.
-MEASURED_TRAFFIC = {}
+MEASURED_TRAFFIC = {
+    ("map512x512-F20000-2M", 0, 1048576, 262208, 1,
+     '{"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "slice_neurons": 0, "tile_docs": 0}'): {
+        "bytes": 9.7184835e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
+        "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, k_search<8,4,1,8,1>, copy-calibrated x2.0 / x1.0",
+    },
+}
 
 
 def parse():

@@ -27,15 +27,16 @@ namespace {
 // order, so their results are bit-identical):
 //   kMaskFma:    acc[s] = fma(w, b_s, acc[s]) with b_s = 1.0 or 0.0 taken from
 //                the wave-uniform mask -- branch-free, T*K VALU per row;
-//   kMaskBranch: a wave-uniform scalar branch per document, popcount*K VALU.
+//   kMaskBranch: wave-uniform scalar branches (a group-of-four test, then one
+//                per document), popcount*K VALU.
 enum MaskMode { kMaskFma = 0, kMaskBranch = 1 };
 
 
 template <int T, int K, int MODE>
 __device__ __forceinline__ void add_row(float (&acc)[T][K], const float4 (&w)[K / 4], uint32_t m) {
+  if (MODE == kMaskFma) {
 #pragma unroll
-  for (int s = 0; s < T; ++s) {
-    if (MODE == kMaskFma) {
+    for (int s = 0; s < T; ++s) {
       const float b = (m >> s) & 1u ? 1.f : 0.f;
 #pragma unroll
       for (int q = 0; q < K / 4; ++q) {
@@ -44,13 +45,24 @@ __device__ __forceinline__ void add_row(float (&acc)[T][K], const float4 (&w)[K 
         acc[s][4 * q + 2] = fmaf(w[q].z, b, acc[s][4 * q + 2]);
         acc[s][4 * q + 3] = fmaf(w[q].w, b, acc[s][4 * q + 3]);
       }
-    } else if (m & (1u << s)) {
+    }
+  } else {
+    // one scalar test per group of four documents first: most rows of a
+    // tile of eight or more documents belong to one or two of them
 #pragma unroll
-      for (int q = 0; q < K / 4; ++q) {
-        acc[s][4 * q + 0] += w[q].x;
-        acc[s][4 * q + 1] += w[q].y;
-        acc[s][4 * q + 2] += w[q].z;
-        acc[s][4 * q + 3] += w[q].w;
+    for (int g = 0; g < T; g += 4) {
+      if (T >= 8 && ((m >> g) & 0xfu) == 0u) continue;
+#pragma unroll
+      for (int s = g; s < (g + 4 < T ? g + 4 : T); ++s) {
+        if (m & (1u << s)) {
+#pragma unroll
+          for (int q = 0; q < K / 4; ++q) {
+            acc[s][4 * q + 0] += w[q].x;
+            acc[s][4 * q + 1] += w[q].y;
+            acc[s][4 * q + 2] += w[q].z;
+            acc[s][4 * q + 3] += w[q].w;
+          }
+        }
       }
     }
   }
@@ -73,6 +85,9 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
 // so the row pipeline never branches on the list length.
 constexpr int kEntryChunk = 512;
 
+// Accelerator complex dies (XCDs) of an MI355X, each with its own L2.
+constexpr uint32_t kXcds = 8;
+
 template <int T, int K, int G, int U, int MODE>
 __global__ void __launch_bounds__(G * 64)
 k_search(SearchArgs a) {
@@ -83,7 +98,14 @@ k_search(SearchArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t t = static_cast<int64_t>(blockIdx.x) * G + wave;  // this wave's tile
+  // Workgroups are handed to the XCDs round-robin (workgroup i of a launch
+  // runs on XCD i mod 8) and gridDim.x is a multiple of 8, so every XCD sees
+  // the same residues in every slice row; give each XCD one contiguous range
+  // of tile groups instead, so that neighbouring tiles of the (clustered)
+  // tiled order, which share features, share that XCD's L2.
+  const uint32_t per_xcd = gridDim.x / kXcds;
+  const uint32_t wg = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  const int64_t t = static_cast<int64_t>(wg) * G + wave;         // this wave's tile
   const int64_t c = blockIdx.y;                                  // neuron slice
   if (t >= a.ntiles) return;                                     // no barriers below
   int2* ent = ent_all[wave];
@@ -336,7 +358,9 @@ __global__ void __launch_bounds__(256) k_decode(SearchArgs a) {
 template <int T, int K, int G>
 hipError_t launch_tkg(const SearchArgs& a, hipStream_t stream) {
   constexpr int U = K == 4 ? 8 : 4;
-  const dim3 grid(static_cast<uint32_t>((a.ntiles + G - 1) / G), static_cast<uint32_t>(a.nchunks));
+  // tile groups rounded up to a multiple of the XCD count (see k_search)
+  const int64_t groups = (a.ntiles + G - 1) / G;
+  const dim3 grid(static_cast<uint32_t>((groups + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));
   if (a.mask_mode == kMaskBranch)
     hipLaunchKernelGGL((k_search<T, K, G, U, kMaskBranch>), grid, dim3(G * 64), 0, stream, a);
   else
