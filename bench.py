@@ -32,7 +32,7 @@ HBM_PEAK_BPS = 8.0e12
 MEASURED_TRAFFIC = {
     ("map512x512-F20000-2M", 0, 1048576, 262208, 1,
      '{"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "slice_neurons": 0, "tile_docs": 0}'): {
-        "bytes": 9.7184835e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
+        "bytes": 9.7151553e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
         "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, k_search<8,4,1,8,1>, copy-calibrated x2.0 / x1.0",
     },
 }
@@ -54,6 +54,7 @@ def parse():
     p.add_argument("--mask-mode", type=int, default=0)
     p.add_argument("--slice-neurons", type=int, default=0)
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage")
+    p.add_argument("--top2", action="store_true", help="search the best and second-best unit")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     p.add_argument("--check-docs", type=int, default=64, help="documents checked against the oracle")
     p.add_argument("--quiet", action="store_true")
@@ -115,6 +116,8 @@ def main():
     norms = torch.empty(N, dtype=torch.float32, device=dev)
     bmu = torch.empty(B, dtype=torch.int32, device=dev)
     dist = torch.empty(B, dtype=torch.float32, device=dev)
+    bmu2 = torch.empty(B, dtype=torch.int32, device=dev) if args.top2 else None
+    dist2 = torch.empty(B, dtype=torch.float32, device=dev) if args.top2 else None
     perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
     knobs = dict(kernel=args.kernel, tile_docs=args.tile_docs, lane_neurons=args.lane_neurons,
                  group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons)
@@ -141,7 +144,11 @@ def main():
         plan = som.som_plan(ip, ix, F, perm=perm, plan=plan_buf, **knobs)
         if ev:
             ev[3].record(stream)
-        som.som_bmu_search_planned(Wd, norms, ip, plan, N=N, bmu=bmu, dist=dist, ws=s_ws)
+        if args.top2:
+            som.som_bmu_search_top2_planned(Wd, norms, ip, plan, N=N, bmu=bmu, dist=dist, bmu2=bmu2,
+                                            dist2=dist2, ws=s_ws)
+        else:
+            som.som_bmu_search_planned(Wd, norms, ip, plan, N=N, bmu=bmu, dist=dist, ws=s_ws)
         if ev:
             ev[4].record(stream)
         return plan
@@ -170,7 +177,8 @@ def main():
     else:
         cnt = som.som_group_plan(ip, ix, F, T, perm=perm)[1]
     union_total = int(cnt.to(torch.int64).sum().item())
-    measured = MEASURED_TRAFFIC.get((cfg.name, args.batch, B, ldw, kernel, json.dumps(knobs, sort_keys=True)))
+    measured = None if args.top2 else MEASURED_TRAFFIC.get((cfg.name, args.batch, B, ldw, kernel,
+                                                             json.dumps(knobs, sort_keys=True)))
     pairs = B * N
     value = pairs / (ms_step * 1e-3)
     search_s = st[3] * 1e-3
@@ -183,6 +191,8 @@ def main():
     import oracle
     bmu_h = bmu.cpu().numpy()
     dist_h = dist.cpu().numpy()
+    bmu2_h = bmu2.cpu().numpy() if args.top2 else None
+    dist2_h = dist2.cpu().numpy() if args.top2 else None
     t = time.time()
     norms64 = oracle.codebook_norms_blocks(W[a:a + 500] for a in range(0, F, 500))
     oracle_norm_s = time.time() - t
@@ -191,7 +201,11 @@ def main():
     bad = 0
     for d in check:
         feats = indices[indptr[d]:indptr[d + 1]].astype(np.int64)
-        ok, why = oracle.accept_bmu(W, norms64, feats, int(bmu_h[d]), float(dist_h[d]))
+        if args.top2:
+            ok, why = oracle.accept_top2(W, norms64, feats, int(bmu_h[d]), float(dist_h[d]), int(bmu2_h[d]),
+                                         float(dist2_h[d]))
+        else:
+            ok, why = oracle.accept_bmu(W, norms64, feats, int(bmu_h[d]), float(dist_h[d]))
         if not ok:
             bad += 1
             log(args, f"doc {d}: {why}")
@@ -230,6 +244,7 @@ def main():
                          f"batch {args.batch}: {B} binary documents, nnz={nnz}"),
             "N": N, "F": F, "ldw": ldw, "B": B, "nnz": nnz, "docs_per_union_sweep": T,
             "knobs": {k: (v or "auto") for k, v in knobs.items()}, "clustered": perm is not None,
+            "second_best_unit": bool(args.top2),
             "bmu_pass_ms": float(st[1] + st[2] + st[3]),
         },
         "roofline": {

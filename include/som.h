@@ -133,6 +133,24 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
                           const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Best AND second-best unit of each document in the same fused pass (the
+ * paper's kernel keeps the second-best unit because the topographic error,
+ * on which both of its stopping rules depend, needs it: Section 6.2, Table 5;
+ * Section 7.2, Table 8).  Arguments as for som_bmu_search, plus
+ *   bmu2    int32 [B] output: argmin over j != bmu[i] of d_j (lowest index on
+ *           exact ties, so with two neurons at the minimum distance, bmu is
+ *           the lower and bmu2 the higher index); -1 when N == 1
+ *   dist2   fp32 [B] output: d_bmu2 as for dist; +inf when N == 1
+ * bmu and dist are identical to som_bmu_search's.  Each neuron slice folds
+ * its own two smallest packed keys into the document's (best, second) pair
+ * with two 64-bit atomic minima; the pair is exact whatever their order.
+ * The workspace size is the same as for som_bmu_search. */
+som_status som_bmu_search_top2(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                               const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                               const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2,
+                               float* dist2, const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
 /* The two stages of som_bmu_search, for callers that search one batch against
  * several codebook versions (a training loop): the plan depends only on the
  * batch, perm and opts, never on the codebook.
@@ -140,7 +158,9 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
  *                       som_plan_bytes(B, nnz, opts) bytes, 256-byte aligned)
  *   som_bmu_search_planned  searches with it; indptr, perm and opts must be those
  *                       the plan was built with; ws holds the per-document
- *                       packed minima (som_bmu_search_planned_workspace_bytes) */
+ *                       packed minima, best and second best
+ *                       (som_bmu_search_planned_workspace_bytes, 16 B per
+ *                       document) */
 size_t som_plan_bytes(int64_t B, int64_t nnz, const som_bmu_opts* opts);
 som_status som_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                     int64_t nnz, const int32_t* perm, const som_bmu_opts* opts, void* plan,
@@ -152,6 +172,14 @@ som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t 
                                   size_t plan_bytes, int32_t* bmu, float* dist,
                                   const som_bmu_opts* opts, void* ws, size_t ws_bytes,
                                   hipStream_t stream);
+/* som_bmu_search_top2 on a plan from som_plan (same rules as
+ * som_bmu_search_planned; the plan does not depend on the top-2 choice). */
+som_status som_bmu_search_top2_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
+                                       const float* norms, const int32_t* indptr, int64_t B,
+                                       int64_t nnz, const int32_t* perm, const void* plan,
+                                       size_t plan_bytes, int32_t* bmu, float* dist, int32_t* bmu2,
+                                       float* dist2, const som_bmu_opts* opts, void* ws,
+                                       size_t ws_bytes, hipStream_t stream);
 
 /* Tile plan of kernel 1 (Section 4.1), written to explicit arrays: for each
  * tile of T consecutive documents of the tiled order (perm as in

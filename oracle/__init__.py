@@ -20,4 +20,5 @@ from .bmu import (  # noqa: F401
     tile_union,
     cluster_order,
     accept_bmu,
+    accept_top2,
 )

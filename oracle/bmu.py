@@ -274,3 +274,39 @@ def accept_bmu(W: np.ndarray, norms: np.ndarray, feats: np.ndarray, g: int, dist
     if abs(float(dist_g) - dd[g]) > rel * ref:
         return False, f"distance {dist_g!r} vs oracle {dd[g]!r} (reference {ref!r})"
     return True, ""
+
+
+def accept_top2(W: np.ndarray, norms: np.ndarray, feats: np.ndarray, g1: int, dist1: float, g2: int,
+                dist2: float, rel: float = 1e-5, N: Optional[int] = None) -> Tuple[bool, str]:
+    """Check one device answer (best g1, second g2) for one document.
+
+    The second-best unit is the best neuron other than the best one (paper,
+    Section 6.2, Table 5: it feeds the topographic error).  g1 must pass
+    ``accept_bmu``; g2 must differ from g1 and be the oracle's best neuron
+    other than g1, or lie within its near-tie band (rel relative); dist2 is
+    checked against d[g2] by the same distance rule as dist1.  With N == 1
+    there is no second unit: g2 must be -1 and dist2 +inf.
+    """
+    n = norms.shape[0] if N is None else int(N)
+    ok, why = accept_bmu(W, norms, feats, g1, dist1, rel, n)
+    if not ok:
+        return False, "first: " + why
+    if n == 1:
+        if g2 == -1 and np.isinf(dist2) and dist2 > 0:
+            return True, ""
+        return False, f"N == 1 needs (-1, inf), got ({g2}, {dist2!r})"
+    if not (0 <= g2 < n) or g2 == g1:
+        return False, f"second index {g2} invalid (first is {g1})"
+    dd = doc_distances(W, norms, feats, n)
+    rest = dd.copy()
+    rest[g1] = np.inf
+    s = int(np.argmin(rest))
+    if g2 != s and not dd[g2] <= dd[s] + rel * abs(dd[s]):
+        return False, f"second {g2} (d={dd[g2]!r}) outside near-tie band of {s} (d={dd[s]!r})"
+    dot_g = (float(feats.size) + float(norms[g2]) - dd[g2]) / 2.0
+    scale = float(feats.size) + float(norms[g2]) + 2.0 * abs(dot_g)
+    ref = abs(dd[g2]) if abs(dd[g2]) >= 1e-3 * scale else scale
+    if abs(float(dist2) - dd[g2]) > rel * ref:
+        return False, f"second distance {dist2!r} vs oracle {dd[g2]!r} (reference {ref!r})"
+    return True, ""
+

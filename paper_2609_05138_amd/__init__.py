@@ -13,6 +13,8 @@ from .som import (  # noqa: F401
     Plan,
     som_bmu_search,
     som_bmu_search_planned,
+    som_bmu_search_top2,
+    som_bmu_search_top2_planned,
     som_bmu_search_planned_workspace_bytes,
     som_bmu_workspace_bytes,
     som_group_plan,

@@ -145,7 +145,10 @@ PlanLayout plan_layout(const Plan& p, int64_t nnz) {
   return l;
 }
 
-size_t keys_bytes(int64_t B) { return som::align_up(sizeof(uint64_t) * (B ? B : 1), 256); }
+// Packed keys: best [B] then second best [B] (the second array is used by
+// the top-2 searches only), each 256-byte aligned.
+size_t keys_half_bytes(int64_t B) { return som::align_up(sizeof(uint64_t) * (B ? B : 1), 256); }
+size_t keys_bytes(int64_t B) { return 2 * keys_half_bytes(B); }
 
 // Workspace of som_bmu_search: the plan, a validation flag and scratch, the keys.
 struct SearchWs {
@@ -200,8 +203,8 @@ hipError_t build_plan(const int32_t* indptr, const int32_t* indices, int64_t B, 
 
 som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
                        const int32_t* indptr, int64_t B, const int32_t* perm, const void* plan,
-                       const PlanLayout& l, int32_t* bmu, float* dist, const Plan& p, uint64_t* keys,
-                       hipStream_t stream) {
+                       const PlanLayout& l, int32_t* bmu, float* dist, int32_t* bmu2, float* dist2,
+                       const Plan& p, uint64_t* keys, hipStream_t stream) {
   som::SearchArgs a{};
   a.W = W;
   a.F = F;
@@ -233,6 +236,11 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
   a.keys = keys;
   a.bmu = bmu;
   a.dist = dist;
+  if (bmu2) {
+    a.keys2 = keys + keys_half_bytes(B) / sizeof(uint64_t);
+    a.bmu2 = bmu2;
+    a.dist2 = dist2;
+  }
   hipError_t e = som::launch_search(a, stream);
   if (e != hipSuccess) return hip_fail(e, "search launch");
   e = som::launch_merge(a, stream);
@@ -244,7 +252,7 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 5; }
+int32_t som_abi_version(void) { return 6; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -272,16 +280,18 @@ size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz, con
   return search_ws(p, B, nnz, opts && opts->validate).total;
 }
 
-som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
-                          const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
-                          const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
-                          void* ws, size_t ws_bytes, hipStream_t stream) {
+static som_status search_impl(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                              const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                              const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2, float* dist2,
+                              bool top2, const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
   som_status s = check_codebook(W, F, N, ldw);
   if (s != SOM_OK) return s;
   if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
   s = check_batch(indptr, indices, B, nnz);
   if (s != SOM_OK) return s;
   if (B > 0 && (!bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "bmu or dist is NULL");
+  if (top2 && B > 0 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "bmu2 or dist2 is NULL");
   Plan p;
   s = make_plan(N, B, opts, &p);
   if (s != SOM_OK) return s;
@@ -298,9 +308,27 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
   }
   hipError_t e = build_plan(indptr, indices, B, F, perm, p, ws, w.plan, stream);
   if (e != hipSuccess) return hip_fail(e, "plan launch");
-  return run_planned(W, F, N, ldw, norms, indptr, B, perm, ws, w.plan, bmu, dist, p,
-                     at<uint64_t>(ws, w.keys), stream);
+  return run_planned(W, F, N, ldw, norms, indptr, B, perm, ws, w.plan, bmu, dist, top2 ? bmu2 : nullptr,
+                     dist2, p, at<uint64_t>(ws, w.keys), stream);
 }
+
+som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                          const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                          const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  return search_impl(W, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, nullptr, nullptr, false,
+                     opts, ws, ws_bytes, stream);
+}
+
+som_status som_bmu_search_top2(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                               const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                               const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2, float* dist2,
+                               const som_bmu_opts* opts, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return search_impl(W, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, bmu2, dist2, true,
+                     opts, ws, ws_bytes, stream);
+}
+
+
 
 size_t som_plan_bytes(int64_t B, int64_t nnz, const som_bmu_opts* opts) {
   if (B < 0 || nnz < 0) return 0;
@@ -337,12 +365,11 @@ size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bm
   return keys_bytes(B);
 }
 
-som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
-                                  const float* norms, const int32_t* indptr, int64_t B,
-                                  int64_t nnz, const int32_t* perm, const void* plan,
-                                  size_t plan_bytes, int32_t* bmu, float* dist,
-                                  const som_bmu_opts* opts, void* ws, size_t ws_bytes,
-                                  hipStream_t stream) {
+static som_status planned_impl(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                               const int32_t* indptr, int64_t B, int64_t nnz, const int32_t* perm,
+                               const void* plan, size_t plan_bytes, int32_t* bmu, float* dist,
+                               int32_t* bmu2, float* dist2, bool top2, const som_bmu_opts* opts, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
   som_status s = check_codebook(W, F, N, ldw);
   if (s != SOM_OK) return s;
   if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
@@ -355,6 +382,7 @@ som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t 
   const PlanLayout l = plan_layout(p, nnz);
   if (B == 0) return ok();
   if (!indptr || !bmu || !dist || !plan) return fail(SOM_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (top2 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "bmu2 or dist2 is NULL");
   if (!aligned(plan, 256)) return fail(SOM_ERR_INVALID_ARG, "plan must be 256-byte aligned");
   if (plan_bytes < l.total)
     return fail(SOM_ERR_INVALID_ARG, "plan buffer smaller than this batch's plan: need " + std::to_string(l.total) + " bytes");
@@ -362,9 +390,31 @@ som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t 
   if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
   if (ws_bytes < keys_bytes(B))
     return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(keys_bytes(B)) + " bytes");
-  return run_planned(W, F, N, ldw, norms, indptr, B, perm, plan, l, bmu, dist, p,
-                     static_cast<uint64_t*>(ws), stream);
+  return run_planned(W, F, N, ldw, norms, indptr, B, perm, plan, l, bmu, dist, top2 ? bmu2 : nullptr, dist2,
+                     p, static_cast<uint64_t*>(ws), stream);
 }
+
+som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
+                                  const float* norms, const int32_t* indptr, int64_t B,
+                                  int64_t nnz, const int32_t* perm, const void* plan,
+                                  size_t plan_bytes, int32_t* bmu, float* dist,
+                                  const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                  hipStream_t stream) {
+  return planned_impl(W, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist, nullptr, nullptr,
+                      false, opts, ws, ws_bytes, stream);
+}
+
+som_status som_bmu_search_top2_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
+                                       const float* norms, const int32_t* indptr, int64_t B,
+                                       int64_t nnz, const int32_t* perm, const void* plan,
+                                       size_t plan_bytes, int32_t* bmu, float* dist, int32_t* bmu2,
+                                       float* dist2, const som_bmu_opts* opts, void* ws,
+                                       size_t ws_bytes, hipStream_t stream) {
+  return planned_impl(W, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist, bmu2, dist2,
+                      true, opts, ws, ws_bytes, stream);
+}
+
+
 
 som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                          int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,

@@ -73,6 +73,7 @@ struct SearchArgs {
   const int32_t* union_feat;
   const uint32_t* union_mask;
   uint64_t* keys;   // [B] packed (distance, index) minima, tiled order
+  uint64_t* keys2;  // [B] second-smallest keys, or nullptr when only the BMU is wanted
   // documents-on-lanes search (kernel 2)
   int kernel;       // 1 = neurons on lanes (tile masks), 2 = documents on lanes (groups)
   int slice;        // kernel 2: neurons per slice (32 or 64)
@@ -82,6 +83,8 @@ struct SearchArgs {
   const int32_t* entry_pos;
   int32_t* bmu;
   float* dist;
+  int32_t* bmu2;    // with keys2: second-best unit (-1 if none) and its distance (+inf)
+  float* dist2;
 };
 
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream);

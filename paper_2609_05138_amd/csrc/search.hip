@@ -79,6 +79,51 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
   return k;
 }
 
+// The two smallest of all lanes' (k1 < k2) pairs: merging two sorted pairs
+// keeps min(a1, b1) and min(max(a1, b1), min(a2, b2)).  Keys are distinct
+// (the low word is the neuron index), so the result is exact.
+__device__ __forceinline__ void wave_top2_u64(uint64_t& k1, uint64_t& k2) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint64_t o1 = (static_cast<uint64_t>(__shfl_xor(static_cast<uint32_t>(k1 >> 32), off, 64)) << 32) |
+                        __shfl_xor(static_cast<uint32_t>(k1), off, 64);
+    const uint64_t o2 = (static_cast<uint64_t>(__shfl_xor(static_cast<uint32_t>(k2 >> 32), off, 64)) << 32) |
+                        __shfl_xor(static_cast<uint32_t>(k2), off, 64);
+    const uint64_t lo = k1 < o1 ? k1 : o1;
+    const uint64_t hi = k1 < o1 ? o1 : k1;
+    const uint64_t m2 = k2 < o2 ? k2 : o2;
+    k1 = lo;
+    k2 = hi < m2 ? hi : m2;
+  }
+}
+
+// Insert a candidate key into a lane's sorted (k1 < k2) pair.
+__device__ __forceinline__ void top2_insert(uint64_t key, uint64_t& k1, uint64_t& k2) {
+  // selects only (a branchy form makes the compiler keep the pair in scratch)
+  const uint64_t lo = key < k1 ? key : k1;
+  const uint64_t hi = key < k1 ? k1 : key;
+  k2 = hi < k2 ? hi : k2;
+  k1 = lo;
+}
+
+// atomicMin on `best`, returning max(previous value, k1): the key this
+// update pushes towards the second place.
+__device__ __forceinline__ uint64_t top2_displaced(uint64_t* best, uint64_t k1) {
+  const uint64_t old = atomicMin(reinterpret_cast<unsigned long long*>(best), static_cast<unsigned long long>(k1));
+  return old > k1 ? old : k1;
+}
+
+// Fold one slice's (k1 < k2) into a document's global pair (best, second).
+// The displaced value max(old best, k1) and k2 are the only keys of this
+// slice that can be the global second: whichever of the two slices holding
+// the global first and second updates `best` later pushes the other into
+// `second`, whatever the order of the atomics, so the final pair is exact.
+__device__ __forceinline__ void top2_merge(uint64_t* best, uint64_t* second, uint64_t k1, uint64_t k2) {
+  const uint64_t displaced = top2_displaced(best, k1);
+  const uint64_t cand = displaced < k2 ? displaced : k2;
+  if (cand != kNoKey) atomicMin(reinterpret_cast<unsigned long long*>(second), static_cast<unsigned long long>(cand));
+}
+
 // Each wave stages its tile's union list in its own LDS window, kEntryChunk
 // entries (feature id, mask) at a time, then issues its row loads from
 // scalar registers.  The window is padded with (row 0, empty mask) entries
@@ -188,6 +233,21 @@ k_search(SearchArgs a) {
     if (p >= a.B) break;
     const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
     const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
+    if (a.keys2) {  // best and second best (wave-uniform branch)
+      uint64_t k1 = kNoKey, k2 = kNoKey;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t j = n0 + 256 * q + 4 * lane + e;
+          if (j < a.N)
+            top2_insert(pack_key(fmaf(-2.f, acc[s][4 * q + e], nnz + nrm[4 * q + e]), static_cast<uint32_t>(j)),
+                        k1, k2);
+        }
+      wave_top2_u64(k1, k2);
+      if (lane == 0) top2_merge(a.keys + p, a.keys2 + p, k1, k2);
+      continue;
+    }
     float best = 0.f;
     uint32_t bj = 0xffffffffu;
 #pragma unroll
@@ -322,6 +382,23 @@ k_search_docs(SearchArgs a) {
 
   if (!valid) return;
   const float nnz = static_cast<float>(e1 - e0);
+  if (a.keys2) {  // best and second best
+    uint64_t k1 = kNoKey, k2 = kNoKey;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int64_t gj = n0 + j;
+      if (gj < a.N) top2_insert(pack_key(fmaf(-2.f, acc[j], nnz + a.norms[gj]), static_cast<uint32_t>(gj)), k1, k2);
+    }
+    // a stale read of `best` only filters: if k1 is not below it, the true
+    // best is below k1 too, so the displaced key would be k1 itself
+    uint64_t* kb = a.keys + p;
+    const uint64_t displaced =
+        k1 < *kb ? top2_displaced(kb, k1) : k1;
+    const uint64_t cand = displaced < k2 ? displaced : k2;
+    uint64_t* ks = a.keys2 + p;
+    if (cand < *ks) atomicMin(reinterpret_cast<unsigned long long*>(ks), static_cast<unsigned long long>(cand));
+    return;
+  }
   float best = 0.f;
   uint32_t bj = 0xffffffffu;
 #pragma unroll
@@ -340,9 +417,13 @@ k_search_docs(SearchArgs a) {
   if (key < *kp) atomicMin(kp, static_cast<unsigned long long>(key));
 }
 
-__global__ void __launch_bounds__(256) k_keys_init(uint64_t* __restrict__ keys, int64_t n) {
+__global__ void __launch_bounds__(256) k_keys_init(uint64_t* __restrict__ keys, uint64_t* __restrict__ keys2,
+                                                   int64_t n) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) keys[i] = kNoKey;
+  if (i < n) {
+    keys[i] = kNoKey;
+    if (keys2) keys2[i] = kNoKey;
+  }
 }
 
 // Decode each document's key into (bmu, dist) in input order.
@@ -353,6 +434,11 @@ __global__ void __launch_bounds__(256) k_decode(SearchArgs a) {
   const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
   a.bmu[d] = static_cast<int32_t>(static_cast<uint32_t>(best));
   a.dist[d] = from_ordered_bits(static_cast<uint32_t>(best >> 32));
+  if (a.keys2) {
+    const uint64_t second = a.keys2[p];
+    a.bmu2[d] = second == kNoKey ? -1 : static_cast<int32_t>(static_cast<uint32_t>(second));
+    a.dist2[d] = second == kNoKey ? __builtin_inff() : from_ordered_bits(static_cast<uint32_t>(second >> 32));
+  }
 }
 
 template <int T, int K, int G>
@@ -411,7 +497,7 @@ hipError_t launch_docs(const SearchArgs& a, hipStream_t stream) {
 
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(k_keys_init, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream,
-                     a.keys, a.B);
+                     a.keys, a.keys2, a.B);
   if (a.kernel == 2) return launch_docs(a, stream);
   switch (a.T) {
     case 1: return a.K == 4 ? launch_tk<1, 4>(a, stream) : launch_tk<1, 8>(a, stream);

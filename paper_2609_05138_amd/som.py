@@ -29,10 +29,12 @@ EXPORTS = (
     "som_codebook_ldw",
     "som_bmu_workspace_bytes",
     "som_bmu_search",
+    "som_bmu_search_top2",
     "som_plan_bytes",
     "som_plan",
     "som_bmu_search_planned_workspace_bytes",
     "som_bmu_search_planned",
+    "som_bmu_search_top2_planned",
     "som_tile_plan",
     "som_group_plan",
     "som_cluster_workspace_bytes",
@@ -96,6 +98,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.som_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
     lib.som_bmu_search_planned_workspace_bytes.restype = _sz
     lib.som_bmu_search_planned_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(som_bmu_opts)]
+    lib.som_bmu_search_top2.restype = _i32
+    lib.som_bmu_search_top2.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp,
+                                        ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
+    lib.som_bmu_search_top2_planned.restype = _i32
+    lib.som_bmu_search_top2_planned.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _i64, _i64, _vp, _vp, _sz,
+                                                _vp, _vp, _vp, _vp, ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
     lib.som_bmu_search_planned.restype = _i32
     lib.som_bmu_search_planned.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _i64, _i64, _vp, _vp, _sz,
                                            _vp, _vp, ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
@@ -182,14 +190,19 @@ def som_bmu_workspace_bytes(F: int, N: int, B: int, nnz: int, validate=False, **
     return int(load().som_bmu_workspace_bytes(F, N, B, nnz, ctypes.byref(o)))
 
 
-def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, indices: torch.Tensor,
-                   N: Optional[int] = None, perm: Optional[torch.Tensor] = None, validate: bool = False,
-                   bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None,
-                   ws: Optional[torch.Tensor] = None, stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
-    """BMU index (int32) and squared distance (fp32) of every CSR document.
+def _outputs(B, device, pairs):
+    out = []
+    for t, dtype, name in pairs:
+        if t is None:
+            t = torch.empty(B, dtype=dtype, device=device)
+        _dev(t, dtype, name)
+        if t.numel() < B:
+            raise ValueError(f"{name} is too small")
+        out.append(t)
+    return out
 
-    ``knobs``: kernel, tile_docs, lane_neurons, group_tiles, mask_mode,
-    slice_neurons (fields of som_bmu_opts; none changes a result)."""
+
+def _search(top2, W, norms, indptr, indices, N, perm, validate, outs, ws, stream, knobs):
     lib = load()
     _dev(W, torch.float32, "W")
     _dev(norms, torch.float32, "norms")
@@ -203,23 +216,42 @@ def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, i
         _dev(perm, torch.int32, "perm")
         if perm.numel() != B:
             raise ValueError("perm must have B entries")
-    if bmu is None:
-        bmu = torch.empty(B, dtype=torch.int32, device=W.device)
-    if dist is None:
-        dist = torch.empty(B, dtype=torch.float32, device=W.device)
-    _dev(bmu, torch.int32, "bmu")
-    _dev(dist, torch.float32, "dist")
-    if bmu.numel() < B or dist.numel() < B:
-        raise ValueError("bmu / dist are too small")
+    names = (("bmu", torch.int32), ("dist", torch.float32), ("bmu2", torch.int32), ("dist2", torch.float32))
+    outs = _outputs(B, W.device, [(t, dt, nm) for t, (nm, dt) in zip(outs, names)])
     o = _opts(validate=validate, **knobs)
     need = int(lib.som_bmu_workspace_bytes(F, n, B, nnz, ctypes.byref(o)))
     if ws is None:
         ws = _workspace(need, W.device)
     _dev(ws, torch.uint8, "ws")
-    _check(lib.som_bmu_search(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), _ptr(indices), B, nnz,
-                              _ptr(perm), _ptr(bmu), _ptr(dist), ctypes.byref(o), _ptr(ws),
-                              ws.numel(), _stream(stream)))
-    return bmu, dist
+    common = (_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), _ptr(indices), B, nnz, _ptr(perm))
+    tail = (ctypes.byref(o), _ptr(ws), ws.numel(), _stream(stream))
+    if top2:
+        _check(lib.som_bmu_search_top2(*common, *(_ptr(t) for t in outs), *tail))
+    else:
+        _check(lib.som_bmu_search(*common, *(_ptr(t) for t in outs), *tail))
+    return tuple(outs)
+
+
+def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, indices: torch.Tensor,
+                   N: Optional[int] = None, perm: Optional[torch.Tensor] = None, validate: bool = False,
+                   bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None,
+                   ws: Optional[torch.Tensor] = None, stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
+    """BMU index (int32) and squared distance (fp32) of every CSR document.
+
+    ``knobs``: kernel, tile_docs, lane_neurons, group_tiles, mask_mode,
+    slice_neurons (fields of som_bmu_opts; none changes a result)."""
+    return _search(False, W, norms, indptr, indices, N, perm, validate, (bmu, dist), ws, stream, knobs)
+
+
+def som_bmu_search_top2(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, indices: torch.Tensor,
+                        N: Optional[int] = None, perm: Optional[torch.Tensor] = None, validate: bool = False,
+                        bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None,
+                        bmu2: Optional[torch.Tensor] = None, dist2: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None, stream=None, **knobs):
+    """(bmu, dist, bmu2, dist2): best and second-best unit of every document
+    (bmu2 = -1 and dist2 = +inf when N == 1)."""
+    return _search(True, W, norms, indptr, indices, N, perm, validate, (bmu, dist, bmu2, dist2), ws, stream,
+                   knobs)
 
 
 class Plan:
@@ -258,11 +290,7 @@ def som_bmu_search_planned_workspace_bytes(N: int, B: int, **knobs) -> int:
     return int(load().som_bmu_search_planned_workspace_bytes(N, B, ctypes.byref(o)))
 
 
-def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, plan: Plan,
-                           N: Optional[int] = None, bmu: Optional[torch.Tensor] = None,
-                           dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                           stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """The search stage on a prebuilt plan (same indptr, perm and knobs)."""
+def _planned(top2, W, norms, indptr, plan, N, outs, ws, stream):
     lib = load()
     _dev(W, torch.float32, "W")
     _dev(norms, torch.float32, "norms")
@@ -272,20 +300,37 @@ def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.T
     B = indptr.numel() - 1
     if B != plan.B:
         raise ValueError("plan was built for another batch")
-    if bmu is None:
-        bmu = torch.empty(B, dtype=torch.int32, device=W.device)
-    if dist is None:
-        dist = torch.empty(B, dtype=torch.float32, device=W.device)
-    _dev(bmu, torch.int32, "bmu")
-    _dev(dist, torch.float32, "dist")
+    names = (("bmu", torch.int32), ("dist", torch.float32), ("bmu2", torch.int32), ("dist2", torch.float32))
+    outs = _outputs(B, W.device, [(t, dt, nm) for t, (nm, dt) in zip(outs, names)])
     o = _opts(**plan.knobs)
     if ws is None:
         ws = _workspace(lib.som_bmu_search_planned_workspace_bytes(n, B, ctypes.byref(o)), W.device)
     _dev(ws, torch.uint8, "ws")
-    _check(lib.som_bmu_search_planned(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), B, plan.nnz,
-                                      _ptr(plan.perm), _ptr(plan.buf), plan.buf.numel(), _ptr(bmu),
-                                      _ptr(dist), ctypes.byref(o), _ptr(ws), ws.numel(), _stream(stream)))
-    return bmu, dist
+    common = (_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), B, plan.nnz, _ptr(plan.perm), _ptr(plan.buf),
+              plan.buf.numel())
+    tail = (ctypes.byref(o), _ptr(ws), ws.numel(), _stream(stream))
+    if top2:
+        _check(lib.som_bmu_search_top2_planned(*common, *(_ptr(t) for t in outs), *tail))
+    else:
+        _check(lib.som_bmu_search_planned(*common, *(_ptr(t) for t in outs), *tail))
+    return tuple(outs)
+
+
+def som_bmu_search_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, plan: Plan,
+                           N: Optional[int] = None, bmu: Optional[torch.Tensor] = None,
+                           dist: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                           stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """The search stage on a prebuilt plan (same indptr, perm and knobs)."""
+    return _planned(False, W, norms, indptr, plan, N, (bmu, dist), ws, stream)
+
+
+def som_bmu_search_top2_planned(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, plan: Plan,
+                                N: Optional[int] = None, bmu: Optional[torch.Tensor] = None,
+                                dist: Optional[torch.Tensor] = None, bmu2: Optional[torch.Tensor] = None,
+                                dist2: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                                stream=None):
+    """Top-2 search stage on a prebuilt plan: (bmu, dist, bmu2, dist2)."""
+    return _planned(True, W, norms, indptr, plan, N, (bmu, dist, bmu2, dist2), ws, stream)
 
 
 def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs: int = 8,

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 5
+    assert som.som_abi_version() == 6
 
 
 def test_codebook_ldw_is_host_only(lib):
@@ -131,6 +131,37 @@ def test_search_rejects_bad_arguments(lib):
     # an empty batch is a valid no-op that touches nothing
     assert call(B=0, nnz=0, indices=null, bmu=null, dist=null, ws=null, ws_bytes=0)[0] == som.SOM_OK
     assert lib.som_last_error().decode() == ""
+
+
+def test_top2_rejects_bad_arguments(lib):
+    null = None
+    fake = ctypes.c_void_p(0x1000)
+    o = som.som_bmu_opts()
+    args = dict(W=fake, F=8, N=8, ldw=8, norms=fake, indptr=fake, indices=fake, B=4, nnz=10,
+                perm=null, bmu=fake, dist=fake, bmu2=fake, dist2=fake, opts=ctypes.byref(o), ws=fake,
+                ws_bytes=1 << 30, stream=null)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return _status(lib, "som_bmu_search_top2", *a.values())
+
+    for k in ("bmu", "dist", "bmu2", "dist2", "W", "norms"):
+        st, msg = call(**{k: null})
+        assert st == som.SOM_ERR_INVALID_ARG, (k, msg)
+    st, msg = call(ws_bytes=16)
+    assert st == som.SOM_ERR_WORKSPACE and "need" in msg
+    assert call(B=0, nnz=0, indices=null, bmu=null, dist=null, bmu2=null, dist2=null, ws=null,
+                ws_bytes=0)[0] == som.SOM_OK
+    big = 1 << 30
+    # W, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist, bmu2, dist2, opts, ws, ws_bytes, stream
+    st, msg = _status(lib, "som_bmu_search_top2_planned", fake, 8, 8, 8, fake, fake, 4, 10, null, fake, big,
+                      fake, fake, null, fake, ctypes.byref(o), fake, big, null)
+    assert st == som.SOM_ERR_INVALID_ARG and "bmu2" in msg
+    st, _ = _status(lib, "som_bmu_search_top2_planned", fake, 8, 8, 8, fake, fake, 4, 10, null, fake, big,
+                    fake, fake, fake, fake, ctypes.byref(o), fake, 8, null)
+    assert st == som.SOM_ERR_WORKSPACE
+    # the planned workspace holds both key arrays: 16 B per document
+    assert lib.som_bmu_search_planned_workspace_bytes(1024, 1000, ctypes.byref(o)) >= 16 * 1000
 
 
 def test_plan_and_cluster_reject_bad_arguments(lib):

@@ -29,7 +29,7 @@ else:  # collected on CPU-only machines, never run there
 REL = 1e-5
 
 
-def _run(cfg_key, batch, cluster, sample, seed):
+def _run(cfg_key, batch, cluster, sample, seed, top2=False):
     from synth import CONFIGS, codebook, documents
     cfg = CONFIGS[cfg_key]
     dev = torch.device("cuda:0")
@@ -47,6 +47,11 @@ def _run(cfg_key, batch, cluster, sample, seed):
     norms = som.som_codebook_norms(Wd, N=cfg.N)
     perm = som.som_cluster_order(ip, ix, cfg.F) if cluster else None
     bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm)
+    second = None
+    if top2:   # the top-2 search on the same data: same first place, plus the second
+        second = som.som_bmu_search_top2(Wd, norms, ip, ix, N=cfg.N, perm=perm)
+        assert torch.equal(second[0], bmu) and torch.equal(second[1], dist)
+        second = [s.cpu().numpy() for s in second[2:]]
     torch.cuda.synchronize()
     bmu, dist = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
     if perm is not None:
@@ -78,6 +83,9 @@ def _run(cfg_key, batch, cluster, sample, seed):
     for d in docs:
         feats = indices[indptr[d]:indptr[d + 1]].astype(np.int64)
         ok, why = oracle.accept_bmu(W, norms64, feats, int(bmu[d]), float(dist[d]), REL)
+        if ok and second is not None:
+            ok, why = oracle.accept_top2(W, norms64, feats, int(bmu[d]), float(dist[d]), int(second[0][d]),
+                                         float(second[1][d]), REL)
         if not ok:
             bad.append((int(d), why))
     print(f"[cfg{cfg_key}] {len(docs) - len(bad)}/{len(docs)} sampled documents accepted", flush=True)
@@ -91,7 +99,7 @@ def test_config3_map256_first_batch():
 
 
 def test_config4_map512_first_batch():
-    _run(4, 0, cluster=False, sample=300, seed=4)
+    _run(4, 0, cluster=False, sample=300, seed=4, top2=True)
 
 
 def test_config4_map512_ragged_last_batch():

@@ -317,6 +317,37 @@ def test_accept_rule():
     assert not oracle.accept_bmu(W, norms, f01, 3, 1.0)[0]
 
 
+def test_accept_top2_rule():
+    ex = _load("hand_examples.json")["examples"][1]     # B: ties and zeros
+    W = _example_W(ex)
+    norms = oracle.codebook_norms(W)
+    f01, f0 = np.array([0, 1]), np.array([0])
+    acc = lambda *a, **k: oracle.accept_top2(W, norms, *a, **k)[0]   # noqa: E731
+    assert acc(f01, 0, 1.0, 2, 1.0)                  # d = (1, 3/2, 1): tie -> 0 then 2
+    assert acc(f01, 2, 1.0, 0, 1.0)                  # the tie partner first is accepted
+    assert not acc(f01, 0, 1.0, 1, 1.5)              # 1 is not the best other than 0
+    assert not acc(f01, 0, 1.0, 0, 1.0)              # second must differ from first
+    assert not acc(f01, 0, 1.0, 2, 1.0 + 1e-3)       # second distance off
+    assert acc(f01, 0, 1.0, 2, 1.0 + 5e-6)
+    assert not acc(f01, 1, 1.5, 0, 1.0)              # first rejected
+    assert not acc(f01, 0, 1.0, 3, 1.0)              # out of range
+    assert acc(f0, 0, 0.0, 1, 1.5)                   # d = (0, 3/2, 2)
+    assert not acc(f0, 0, 0.0, 2, 2.0)
+    W1 = W[:, :1].copy()
+    n1 = oracle.codebook_norms(W1)
+    assert oracle.accept_top2(W1, n1, f0, 0, 0.0, -1, np.inf)[0]     # N == 1: no second unit
+    assert not oracle.accept_top2(W1, n1, f0, 0, 0.0, 0, 0.0)[0]
+    assert not oracle.accept_top2(W1, n1, f0, 0, 0.0, -1, 5.0)[0]
+    # near-tie band of the second place: d = (0.25, 1, 1 + eps) for one feature
+    for eps, ok in ((1e-6, True), (1e-4, False)):
+        Wn = np.array([[0.5, 0.0, 1.0 - np.sqrt(1.0 + eps)]])
+        nn = oracle.codebook_norms(Wn)
+        d = oracle.doc_distances(Wn, nn, f0)
+        assert abs(d[2] - (1.0 + eps)) < 1e-12
+        assert oracle.accept_top2(Wn, nn, f0, 0, 0.25, 1, 1.0)[0]
+        assert oracle.accept_top2(Wn, nn, f0, 0, 0.25, 2, float(d[2]))[0] == ok
+
+
 def test_rejects_unsorted_documents():
     W = np.ones((4, 2))
     with pytest.raises(ValueError):
