@@ -55,6 +55,8 @@ def parse():
     p.add_argument("--slice-neurons", type=int, default=0)
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage")
     p.add_argument("--top2", action="store_true", help="search the best and second-best unit")
+    p.add_argument("--weights", choices=("f32", "f16"), default="f32",
+                   help="codebook storage (sums are fp32 either way)")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     p.add_argument("--check-docs", type=int, default=64, help="documents checked against the oracle")
     p.add_argument("--quiet", action="store_true")
@@ -111,6 +113,9 @@ def main():
         Wd[r0:r0 + 1024, :N].copy_(Wh[r0:r0 + 1024].to(dev))
     if ldw > N:
         Wd[:, N:].zero_()
+    if args.weights == "f16":          # stored rounded to fp16 on the device
+        Wd = Wd.half()
+        torch.cuda.empty_cache()
     ip = torch.from_numpy(indptr).to(dev)
     ix = torch.from_numpy(indices).to(dev)
     norms = torch.empty(N, dtype=torch.float32, device=dev)
@@ -177,14 +182,15 @@ def main():
     else:
         cnt = som.som_group_plan(ip, ix, F, T, perm=perm)[1]
     union_total = int(cnt.to(torch.int64).sum().item())
-    measured = None if args.top2 else MEASURED_TRAFFIC.get((cfg.name, args.batch, B, ldw, kernel,
-                                                             json.dumps(knobs, sort_keys=True)))
+    measured = None if (args.top2 or args.weights != "f32") else MEASURED_TRAFFIC.get(
+        (cfg.name, args.batch, B, ldw, kernel, json.dumps(knobs, sort_keys=True)))
     pairs = B * N
     value = pairs / (ms_step * 1e-3)
     search_s = st[3] * 1e-3
     # algorithmic L2-level bytes of one search launch: every union row slice
-    # once per tile (kernel 1) or group (kernel 2), plus the norms once per unit
-    l2_bytes = 4.0 * N * (union_total + ntiles)
+    # once per tile (kernel 1) or group (kernel 2), plus the fp32 norms once per unit
+    wbytes = 2.0 if args.weights == "f16" else 4.0
+    l2_bytes = N * (wbytes * union_total + 4.0 * ntiles)
     useful_adds = float(nnz) * N
 
     # spot check of this run's results against the oracle
@@ -193,6 +199,8 @@ def main():
     dist_h = dist.cpu().numpy()
     bmu2_h = bmu2.cpu().numpy() if args.top2 else None
     dist2_h = dist2.cpu().numpy() if args.top2 else None
+    if args.weights == "f16":
+        W = W.astype(np.float16)       # the oracle consumes the stored (rounded) weights
     t = time.time()
     norms64 = oracle.codebook_norms_blocks(W[a:a + 500] for a in range(0, F, 500))
     oracle_norm_s = time.time() - t
@@ -240,11 +248,12 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": (f"{cfg.name}: map {int(round(N ** 0.5))}^2 (N={N}), F={F}, fp32 feature-major codebook; "
+            "workload": (f"{cfg.name}: map {int(round(N ** 0.5))}^2 (N={N}), F={F}, "
+                         f"{'fp16' if args.weights == 'f16' else 'fp32'} feature-major codebook; "
                          f"batch {args.batch}: {B} binary documents, nnz={nnz}"),
             "N": N, "F": F, "ldw": ldw, "B": B, "nnz": nnz, "docs_per_union_sweep": T,
             "knobs": {k: (v or "auto") for k, v in knobs.items()}, "clustered": perm is not None,
-            "second_best_unit": bool(args.top2),
+            "second_best_unit": bool(args.top2), "weights": args.weights,
             "bmu_pass_ms": float(st[1] + st[2] + st[3]),
         },
         "roofline": {

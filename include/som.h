@@ -228,6 +228,46 @@ som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int6
                              int64_t nnz, int32_t* perm, void* ws, size_t ws_bytes,
                              hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * fp16 codebook storage, fp32 accumulation (the paper's kernel stores two
+ * bytes per weight, Section 4.2, and loads them as half-precision pairs,
+ * Section 4.3).  W holds IEEE-754
+ * binary16 bit patterns, feature-major [F][ldw], 16-byte aligned, with
+ * ldw >= N and ldw % 8 == 0 (som_codebook_ldw(N) satisfies both).  Every
+ * other argument, output and error is as for the fp32 function of the same
+ * name.  The results are those of the fp32 functions on the codebook whose
+ * weights are the fp16 values widened exactly to fp32: norms are the rounded
+ * weights' norms (fp64 accumulate, rounded once), and every document's dot
+ * product sums the widened weights in ascending feature order, so fp16 and
+ * fp32 searches of the same (fp16-representable) codebook are bit-identical.
+ * Search knobs: kernel 1 only (kernel 0 or 1), lane_neurons 0 or 8 (a
+ * 512-neuron slice, one 128-bit load of 8 weights per lane per row),
+ * tile_docs up to 16.  Plans from som_plan are shared with the fp32 search.
+ * ------------------------------------------------------------------------- */
+som_status som_codebook_norms_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw, float* norms,
+                                  hipStream_t stream);
+som_status som_bmu_search_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                              const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                              const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+som_status som_bmu_search_top2_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                                   const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                   const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2,
+                                   float* dist2, const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
+som_status som_bmu_search_planned_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw,
+                                      const float* norms, const int32_t* indptr, int64_t B,
+                                      int64_t nnz, const int32_t* perm, const void* plan,
+                                      size_t plan_bytes, int32_t* bmu, float* dist,
+                                      const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                      hipStream_t stream);
+som_status som_bmu_search_top2_planned_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw,
+                                           const float* norms, const int32_t* indptr, int64_t B,
+                                           int64_t nnz, const int32_t* perm, const void* plan,
+                                           size_t plan_bytes, int32_t* bmu, float* dist, int32_t* bmu2,
+                                           float* dist2, const som_bmu_opts* opts, void* ws,
+                                           size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

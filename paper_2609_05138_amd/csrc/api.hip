@@ -39,11 +39,14 @@ const P* at(const void* base, size_t off) {
   return reinterpret_cast<const P*>(static_cast<const char*>(base) + off);
 }
 
-som_status check_codebook(const float* W, int64_t F, int64_t N, int64_t ldw) {
+// One 128-bit load holds 4 fp32 or 8 fp16 weights; rows must start on one.
+som_status check_codebook(const void* W, int weights, int64_t F, int64_t N, int64_t ldw) {
   if (!W) return fail(SOM_ERR_INVALID_ARG, "W is NULL");
   if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
   if (N < 1 || N > kI32Max) return fail(SOM_ERR_INVALID_ARG, "N must be in [1, 2^31)");
   if (ldw < N) return fail(SOM_ERR_INVALID_ARG, "ldw must be >= N");
+  if (weights == som::kWeightsF16 && ldw % 8 != 0)
+    return fail(SOM_ERR_INVALID_ARG, "ldw must be a multiple of 8 for an fp16 codebook");
   if (ldw % 4 != 0) return fail(SOM_ERR_INVALID_ARG, "ldw must be a multiple of 4");
   if (!aligned(W, 16)) return fail(SOM_ERR_INVALID_ARG, "W must be 16-byte aligned");
   return SOM_OK;
@@ -74,9 +77,12 @@ struct Plan {
   int64_t nchunks = 0;  // neuron slices
 };
 
-som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
+som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
+                     int weights = som::kWeightsF32) {
   som_bmu_opts o{};
   if (opts) o = *opts;
+  const bool f16 = weights == som::kWeightsF16;
+  if (f16 && o.kernel == 2) return fail(SOM_ERR_INVALID_ARG, "an fp16 codebook is searched by kernel 1 only");
   if (o.reserved != 0) return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
   if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
   if (o.kernel < 0 || o.kernel > 2) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1 or 2");
@@ -86,9 +92,11 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p) {
     const int T = o.tile_docs ? o.tile_docs : 8;
     if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
       return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 1, 2, 4, 8, 16 or 32");
-    const int K = o.lane_neurons ? o.lane_neurons : 4;
+    if (f16 && T == 32) return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs 32 is not available for an fp16 codebook");
+    const int K = o.lane_neurons ? o.lane_neurons : (f16 ? 8 : 4);
     if (K != 4 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0, 4 or 8");
     if (T == 32 && K != 4) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 4 when tile_docs is 32");
+    if (f16 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0 or 8 for an fp16 codebook");
     const int G = o.group_tiles ? o.group_tiles : 1;
     if (G != 1 && G != 2 && G != 4 && G != 8)
       return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles must be 0, 1, 2, 4 or 8 for kernel 1");
@@ -201,12 +209,13 @@ hipError_t build_plan(const int32_t* indptr, const int32_t* indices, int64_t B, 
                                 at<int32_t>(plan, l.feat), at<int32_t>(plan, l.extra), stream);
 }
 
-som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t ldw, const float* norms,
                        const int32_t* indptr, int64_t B, const int32_t* perm, const void* plan,
                        const PlanLayout& l, int32_t* bmu, float* dist, int32_t* bmu2, float* dist2,
                        const Plan& p, uint64_t* keys, hipStream_t stream) {
   som::SearchArgs a{};
   a.W = W;
+  a.weights = weights;
   a.F = F;
   a.N = N;
   a.ldw = ldw;
@@ -252,7 +261,7 @@ som_status run_planned(const float* W, int64_t F, int64_t N, int64_t ldw, const 
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 6; }
+int32_t som_abi_version(void) { return 7; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -263,14 +272,24 @@ int64_t som_codebook_ldw(int64_t N) {
   return ldw;
 }
 
-som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
-                              hipStream_t stream) {
-  som_status s = check_codebook(W, F, N, ldw);
+static som_status norms_impl(const void* W, int weights, int64_t F, int64_t N, int64_t ldw, float* norms,
+                             hipStream_t stream) {
+  som_status s = check_codebook(W, weights, F, N, ldw);
   if (s != SOM_OK) return s;
   if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
-  hipError_t e = som::launch_norms(W, F, N, ldw, norms, stream);
+  hipError_t e = som::launch_norms(W, weights, F, N, ldw, norms, stream);
   if (e != hipSuccess) return hip_fail(e, "norms launch");
   return ok();
+}
+
+som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
+                              hipStream_t stream) {
+  return norms_impl(W, som::kWeightsF32, F, N, ldw, norms, stream);
+}
+
+som_status som_codebook_norms_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw, float* norms,
+                                  hipStream_t stream) {
+  return norms_impl(W, som::kWeightsF16, F, N, ldw, norms, stream);
 }
 
 size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz, const som_bmu_opts* opts) {
@@ -280,12 +299,12 @@ size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz, con
   return search_ws(p, B, nnz, opts && opts->validate).total;
 }
 
-static som_status search_impl(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
-                              const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
-                              const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2, float* dist2,
-                              bool top2, const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+static som_status search_impl(const void* W, int weights, int64_t F, int64_t N, int64_t ldw,
+                              const float* norms, const int32_t* indptr, const int32_t* indices, int64_t B,
+                              int64_t nnz, const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2,
+                              float* dist2, bool top2, const som_bmu_opts* opts, void* ws, size_t ws_bytes,
                               hipStream_t stream) {
-  som_status s = check_codebook(W, F, N, ldw);
+  som_status s = check_codebook(W, weights, F, N, ldw);
   if (s != SOM_OK) return s;
   if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
   s = check_batch(indptr, indices, B, nnz);
@@ -293,7 +312,7 @@ static som_status search_impl(const float* W, int64_t F, int64_t N, int64_t ldw,
   if (B > 0 && (!bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "bmu or dist is NULL");
   if (top2 && B > 0 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "bmu2 or dist2 is NULL");
   Plan p;
-  s = make_plan(N, B, opts, &p);
+  s = make_plan(N, B, opts, &p, weights);
   if (s != SOM_OK) return s;
   const bool validate = opts && opts->validate;
   const SearchWs w = search_ws(p, B, nnz, validate);
@@ -308,7 +327,7 @@ static som_status search_impl(const float* W, int64_t F, int64_t N, int64_t ldw,
   }
   hipError_t e = build_plan(indptr, indices, B, F, perm, p, ws, w.plan, stream);
   if (e != hipSuccess) return hip_fail(e, "plan launch");
-  return run_planned(W, F, N, ldw, norms, indptr, B, perm, ws, w.plan, bmu, dist, top2 ? bmu2 : nullptr,
+  return run_planned(W, weights, F, N, ldw, norms, indptr, B, perm, ws, w.plan, bmu, dist, top2 ? bmu2 : nullptr,
                      dist2, p, at<uint64_t>(ws, w.keys), stream);
 }
 
@@ -316,16 +335,33 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
                           const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
                           const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
                           void* ws, size_t ws_bytes, hipStream_t stream) {
-  return search_impl(W, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, nullptr, nullptr, false,
-                     opts, ws, ws_bytes, stream);
+  return search_impl(W, som::kWeightsF32, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, nullptr,
+                     nullptr, false, opts, ws, ws_bytes, stream);
 }
 
 som_status som_bmu_search_top2(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
                                const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
                                const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2, float* dist2,
                                const som_bmu_opts* opts, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return search_impl(W, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, bmu2, dist2, true,
-                     opts, ws, ws_bytes, stream);
+  return search_impl(W, som::kWeightsF32, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, bmu2,
+                     dist2, true, opts, ws, ws_bytes, stream);
+}
+
+som_status som_bmu_search_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                              const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                              const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                              void* ws, size_t ws_bytes, hipStream_t stream) {
+  return search_impl(W, som::kWeightsF16, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, nullptr,
+                     nullptr, false, opts, ws, ws_bytes, stream);
+}
+
+som_status som_bmu_search_top2_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                                   const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                   const int32_t* perm, int32_t* bmu, float* dist, int32_t* bmu2,
+                                   float* dist2, const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  return search_impl(W, som::kWeightsF16, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, bmu2,
+                     dist2, true, opts, ws, ws_bytes, stream);
 }
 
 
@@ -365,19 +401,19 @@ size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bm
   return keys_bytes(B);
 }
 
-static som_status planned_impl(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
-                               const int32_t* indptr, int64_t B, int64_t nnz, const int32_t* perm,
-                               const void* plan, size_t plan_bytes, int32_t* bmu, float* dist,
-                               int32_t* bmu2, float* dist2, bool top2, const som_bmu_opts* opts, void* ws,
-                               size_t ws_bytes, hipStream_t stream) {
-  som_status s = check_codebook(W, F, N, ldw);
+static som_status planned_impl(const void* W, int weights, int64_t F, int64_t N, int64_t ldw,
+                               const float* norms, const int32_t* indptr, int64_t B, int64_t nnz,
+                               const int32_t* perm, const void* plan, size_t plan_bytes, int32_t* bmu,
+                               float* dist, int32_t* bmu2, float* dist2, bool top2, const som_bmu_opts* opts,
+                               void* ws, size_t ws_bytes, hipStream_t stream) {
+  som_status s = check_codebook(W, weights, F, N, ldw);
   if (s != SOM_OK) return s;
   if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
   if (B < 0 || B >= kI32Max) return fail(SOM_ERR_INVALID_ARG, "B must be in [0, 2^31 - 1)");
   if (nnz < 0 || nnz > kI32Max) return fail(SOM_ERR_INVALID_ARG, "nnz must be in [0, 2^31)");
   if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on a planned search");
   Plan p;
-  s = make_plan(N, B, opts, &p);
+  s = make_plan(N, B, opts, &p, weights);
   if (s != SOM_OK) return s;
   const PlanLayout l = plan_layout(p, nnz);
   if (B == 0) return ok();
@@ -390,7 +426,7 @@ static som_status planned_impl(const float* W, int64_t F, int64_t N, int64_t ldw
   if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
   if (ws_bytes < keys_bytes(B))
     return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(keys_bytes(B)) + " bytes");
-  return run_planned(W, F, N, ldw, norms, indptr, B, perm, plan, l, bmu, dist, top2 ? bmu2 : nullptr, dist2,
+  return run_planned(W, weights, F, N, ldw, norms, indptr, B, perm, plan, l, bmu, dist, top2 ? bmu2 : nullptr, dist2,
                      p, static_cast<uint64_t*>(ws), stream);
 }
 
@@ -400,8 +436,8 @@ som_status som_bmu_search_planned(const float* W, int64_t F, int64_t N, int64_t 
                                   size_t plan_bytes, int32_t* bmu, float* dist,
                                   const som_bmu_opts* opts, void* ws, size_t ws_bytes,
                                   hipStream_t stream) {
-  return planned_impl(W, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist, nullptr, nullptr,
-                      false, opts, ws, ws_bytes, stream);
+  return planned_impl(W, som::kWeightsF32, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist,
+                      nullptr, nullptr, false, opts, ws, ws_bytes, stream);
 }
 
 som_status som_bmu_search_top2_planned(const float* W, int64_t F, int64_t N, int64_t ldw,
@@ -410,8 +446,28 @@ som_status som_bmu_search_top2_planned(const float* W, int64_t F, int64_t N, int
                                        size_t plan_bytes, int32_t* bmu, float* dist, int32_t* bmu2,
                                        float* dist2, const som_bmu_opts* opts, void* ws,
                                        size_t ws_bytes, hipStream_t stream) {
-  return planned_impl(W, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist, bmu2, dist2,
-                      true, opts, ws, ws_bytes, stream);
+  return planned_impl(W, som::kWeightsF32, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist,
+                      bmu2, dist2, true, opts, ws, ws_bytes, stream);
+}
+
+som_status som_bmu_search_planned_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw,
+                                      const float* norms, const int32_t* indptr, int64_t B,
+                                      int64_t nnz, const int32_t* perm, const void* plan,
+                                      size_t plan_bytes, int32_t* bmu, float* dist,
+                                      const som_bmu_opts* opts, void* ws, size_t ws_bytes,
+                                      hipStream_t stream) {
+  return planned_impl(W, som::kWeightsF16, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist,
+                      nullptr, nullptr, false, opts, ws, ws_bytes, stream);
+}
+
+som_status som_bmu_search_top2_planned_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw,
+                                           const float* norms, const int32_t* indptr, int64_t B,
+                                           int64_t nnz, const int32_t* perm, const void* plan,
+                                           size_t plan_bytes, int32_t* bmu, float* dist, int32_t* bmu2,
+                                           float* dist2, const som_bmu_opts* opts, void* ws,
+                                           size_t ws_bytes, hipStream_t stream) {
+  return planned_impl(W, som::kWeightsF16, F, N, ldw, norms, indptr, B, nnz, perm, plan, plan_bytes, bmu, dist,
+                      bmu2, dist2, true, opts, ws, ws_bytes, stream);
 }
 
 

@@ -34,7 +34,11 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Launchers (each enqueues on `stream` and returns the launch status).
 // ---------------------------------------------------------------------------
 
-hipError_t launch_norms(const float* W, int64_t F, int64_t N, int64_t ldw, float* norms,
+// Codebook storage types (SearchArgs::weights, launch_norms).
+constexpr int kWeightsF32 = 0;
+constexpr int kWeightsF16 = 1;
+
+hipError_t launch_norms(const void* W, int weights, int64_t F, int64_t N, int64_t ldw, float* norms,
                         hipStream_t stream);
 
 // CSR (and optional permutation) checks; sets *flag (device int) nonzero on failure.
@@ -56,7 +60,8 @@ hipError_t launch_group_plan(const int32_t* indptr, const int32_t* indices, int6
                              int32_t* group_feat, int32_t* entry_pos, hipStream_t stream);
 
 struct SearchArgs {
-  const float* W;
+  const void* W;    // fp32 or fp16 [F][ldw] (see `weights`)
+  int weights;      // kWeightsF32 or kWeightsF16 (kernel 1 only)
   int64_t F, N, ldw;
   const float* norms;
   const int32_t* indptr;
@@ -88,6 +93,8 @@ struct SearchArgs {
 };
 
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream);
+// Kernel 1 over an fp16 codebook (its own translation unit).
+hipError_t launch_search_k1_f16(const SearchArgs& a, hipStream_t stream);
 // Initialises the keys, then runs the fused search; launch_merge decodes the
 // keys into results in input order.
 hipError_t launch_merge(const SearchArgs& a, hipStream_t stream);

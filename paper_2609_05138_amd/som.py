@@ -39,6 +39,11 @@ EXPORTS = (
     "som_group_plan",
     "som_cluster_workspace_bytes",
     "som_cluster_order",
+    "som_codebook_norms_f16",
+    "som_bmu_search_f16",
+    "som_bmu_search_top2_f16",
+    "som_bmu_search_planned_f16",
+    "som_bmu_search_top2_planned_f16",
 )
 
 
@@ -113,6 +118,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.som_group_plan.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp]
     lib.som_cluster_workspace_bytes.restype = _sz
     lib.som_cluster_workspace_bytes.argtypes = [_i64, _i64, _i64]
+    # the fp16 functions take the same arguments (W as binary16 bit patterns)
+    for base in ("som_codebook_norms", "som_bmu_search", "som_bmu_search_top2", "som_bmu_search_planned",
+                 "som_bmu_search_top2_planned"):
+        fn = getattr(lib, base + "_f16")
+        fn.restype = _i32
+        fn.argtypes = getattr(lib, base).argtypes
     lib.som_cluster_order.restype = _i32
     lib.som_cluster_order.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _sz, _vp]
     _lib = lib
@@ -138,6 +149,15 @@ def _dev(t: torch.Tensor, dtype, name: str) -> torch.Tensor:
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return t
+
+
+def _codebook(W: torch.Tensor) -> str:
+    """Check the codebook tensor; return the C function suffix for its dtype."""
+    if isinstance(W, torch.Tensor) and W.dtype == torch.float16:
+        _dev(W, torch.float16, "W")
+        return "_f16"
+    _dev(W, torch.float32, "W")
+    return ""
 
 
 def _stream(stream) -> ctypes.c_void_p:
@@ -171,9 +191,9 @@ def som_codebook_ldw(N: int) -> int:
 
 def som_codebook_norms(W: torch.Tensor, N: Optional[int] = None, norms: Optional[torch.Tensor] = None,
                        stream=None) -> torch.Tensor:
-    """||w_j||^2 for j < N of the feature-major codebook W [F, ldw] (fp32)."""
+    """||w_j||^2 for j < N of the feature-major codebook W [F, ldw] (fp32 or fp16)."""
     lib = load()
-    _dev(W, torch.float32, "W")
+    sfx = _codebook(W)
     F, ldw = W.shape
     n = ldw if N is None else int(N)
     if norms is None:
@@ -181,7 +201,7 @@ def som_codebook_norms(W: torch.Tensor, N: Optional[int] = None, norms: Optional
     _dev(norms, torch.float32, "norms")
     if norms.numel() < n:
         raise ValueError("norms is too small")
-    _check(lib.som_codebook_norms(_ptr(W), F, n, ldw, _ptr(norms), _stream(stream)))
+    _check(getattr(lib, "som_codebook_norms" + sfx)(_ptr(W), F, n, ldw, _ptr(norms), _stream(stream)))
     return norms
 
 
@@ -204,7 +224,7 @@ def _outputs(B, device, pairs):
 
 def _search(top2, W, norms, indptr, indices, N, perm, validate, outs, ws, stream, knobs):
     lib = load()
-    _dev(W, torch.float32, "W")
+    sfx = _codebook(W)
     _dev(norms, torch.float32, "norms")
     _dev(indptr, torch.int32, "indptr")
     _dev(indices, torch.int32, "indices")
@@ -226,9 +246,9 @@ def _search(top2, W, norms, indptr, indices, N, perm, validate, outs, ws, stream
     common = (_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), _ptr(indices), B, nnz, _ptr(perm))
     tail = (ctypes.byref(o), _ptr(ws), ws.numel(), _stream(stream))
     if top2:
-        _check(lib.som_bmu_search_top2(*common, *(_ptr(t) for t in outs), *tail))
+        _check(getattr(lib, "som_bmu_search_top2" + sfx)(*common, *(_ptr(t) for t in outs), *tail))
     else:
-        _check(lib.som_bmu_search(*common, *(_ptr(t) for t in outs), *tail))
+        _check(getattr(lib, "som_bmu_search" + sfx)(*common, *(_ptr(t) for t in outs), *tail))
     return tuple(outs)
 
 
@@ -292,7 +312,7 @@ def som_bmu_search_planned_workspace_bytes(N: int, B: int, **knobs) -> int:
 
 def _planned(top2, W, norms, indptr, plan, N, outs, ws, stream):
     lib = load()
-    _dev(W, torch.float32, "W")
+    sfx = _codebook(W)
     _dev(norms, torch.float32, "norms")
     _dev(indptr, torch.int32, "indptr")
     F, ldw = W.shape
@@ -310,9 +330,9 @@ def _planned(top2, W, norms, indptr, plan, N, outs, ws, stream):
               plan.buf.numel())
     tail = (ctypes.byref(o), _ptr(ws), ws.numel(), _stream(stream))
     if top2:
-        _check(lib.som_bmu_search_top2_planned(*common, *(_ptr(t) for t in outs), *tail))
+        _check(getattr(lib, "som_bmu_search_top2_planned" + sfx)(*common, *(_ptr(t) for t in outs), *tail))
     else:
-        _check(lib.som_bmu_search_planned(*common, *(_ptr(t) for t in outs), *tail))
+        _check(getattr(lib, "som_bmu_search_planned" + sfx)(*common, *(_ptr(t) for t in outs), *tail))
     return tuple(outs)
 
 

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 6
+    assert som.som_abi_version() == 7
 
 
 def test_codebook_ldw_is_host_only(lib):
@@ -162,6 +162,27 @@ def test_top2_rejects_bad_arguments(lib):
     assert st == som.SOM_ERR_WORKSPACE
     # the planned workspace holds both key arrays: 16 B per document
     assert lib.som_bmu_search_planned_workspace_bytes(1024, 1000, ctypes.byref(o)) >= 16 * 1000
+
+
+def test_f16_rejects_bad_arguments(lib):
+    null = None
+    fake = ctypes.c_void_p(0x1000)
+    O = som.som_bmu_opts
+
+    def call(ldw=16, opts=None, **kw):
+        o = opts if opts is not None else O()
+        return _status(lib, "som_bmu_search_f16", fake, 8, 12, ldw, fake, fake, fake, 4, 10, null, fake, fake,
+                       ctypes.byref(o), fake, 1 << 30, null)
+
+    st, msg = call(ldw=12)                    # fine for fp32, not for fp16 (8 halves per load)
+    assert st == som.SOM_ERR_INVALID_ARG and "multiple of 8" in msg
+    for bad in (O(2), O(1, 0, 4), O(1, 32), O(1, 32, 4)):
+        st, msg = call(opts=bad)
+        assert st == som.SOM_ERR_INVALID_ARG, msg
+    st, msg = _status(lib, "som_codebook_norms_f16", fake, 8, 12, 12, fake, null)
+    assert st == som.SOM_ERR_INVALID_ARG and "multiple of 8" in msg
+    st, _ = _status(lib, "som_codebook_norms_f16", null, 8, 8, 8, fake, null)
+    assert st == som.SOM_ERR_INVALID_ARG
 
 
 def test_plan_and_cluster_reject_bad_arguments(lib):

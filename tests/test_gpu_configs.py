@@ -29,7 +29,7 @@ else:  # collected on CPU-only machines, never run there
 REL = 1e-5
 
 
-def _run(cfg_key, batch, cluster, sample, seed, top2=False):
+def _run(cfg_key, batch, cluster, sample, seed, top2=False, f16=False):
     from synth import CONFIGS, codebook, documents
     cfg = CONFIGS[cfg_key]
     dev = torch.device("cuda:0")
@@ -52,6 +52,12 @@ def _run(cfg_key, batch, cluster, sample, seed, top2=False):
         second = som.som_bmu_search_top2(Wd, norms, ip, ix, N=cfg.N, perm=perm)
         assert torch.equal(second[0], bmu) and torch.equal(second[1], dist)
         second = [s.cpu().numpy() for s in second[2:]]
+    half = None
+    if f16:    # the same codebook stored in fp16 (rounded on the device), searched as such
+        W16d = Wd.half()
+        n16 = som.som_codebook_norms(W16d, N=cfg.N)
+        half = [x.cpu().numpy() for x in som.som_bmu_search(W16d, n16, ip, ix, N=cfg.N, perm=perm)]
+        del W16d, n16
     torch.cuda.synchronize()
     bmu, dist = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
     if perm is not None:
@@ -89,6 +95,16 @@ def _run(cfg_key, batch, cluster, sample, seed, top2=False):
         if not ok:
             bad.append((int(d), why))
     print(f"[cfg{cfg_key}] {len(docs) - len(bad)}/{len(docs)} sampled documents accepted", flush=True)
+    if half is not None:
+        W16 = W.astype(np.float16)      # the oracle consumes the rounded weights
+        n16_64 = oracle.codebook_norms_blocks(W16[a:a + 500] for a in range(0, cfg.F, 500))
+        for d in docs:
+            feats = indices[indptr[d]:indptr[d + 1]].astype(np.int64)
+            ok, why = oracle.accept_bmu(W16, n16_64, feats, int(half[0][d]), float(half[1][d]), REL)
+            if not ok:
+                bad.append((int(d), "fp16: " + why))
+        print(f"[cfg{cfg_key}] fp16 codebook checked on the same sample", flush=True)
+        del W16
     del W
     gc.collect()
     assert not bad, bad[:5]
@@ -99,7 +115,7 @@ def test_config3_map256_first_batch():
 
 
 def test_config4_map512_first_batch():
-    _run(4, 0, cluster=False, sample=300, seed=4, top2=True)
+    _run(4, 0, cluster=False, sample=300, seed=4, top2=True, f16=True)
 
 
 def test_config4_map512_ragged_last_batch():
