@@ -318,8 +318,13 @@ k_search(SearchArgs a) {
 
 template <typename WT, int T, int K, int G>
 hipError_t launch_tkg(const SearchArgs& a, hipStream_t stream) {
-  // rows per batch: 8 when a row is one 128-bit load per lane, else 4
-  constexpr int U = K / Storage<WT>::kE == 1 ? 8 : 4;
+  // Rows per batch (two batches in flight), chosen by measurement on the
+  // 512^2 map: deeper batches raise each wave's loads in flight but cost
+  // VGPRs, and the occupancy they take matters more.  fp32 with one 128-bit
+  // load per lane per row: 8 rows, 4 from T = 16 on (the accumulators grow);
+  // fp16 (8 weights per load): 4 rows, 2 from T = 16 on; two loads per row: 4.
+  constexpr int Q = K / Storage<WT>::kE;
+  constexpr int U = Q == 1 ? (sizeof(WT) == 2 ? (T >= 16 ? 2 : 4) : (T >= 16 ? 4 : 8)) : 4;
   // tile groups rounded up to a multiple of the XCD count (see k_search)
   const int64_t groups = (a.ntiles + G - 1) / G;
   const dim3 grid(static_cast<uint32_t>((groups + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));

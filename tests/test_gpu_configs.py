@@ -3,8 +3,8 @@
 For the 256^2 and 512^2 maps (N = 65,536 and 262,144 neurons, F = 20,000,
 codebooks of 5.2 and 21 GB) the oracle cannot score a whole batch, so each
 test runs the device search on a full batch in the launch configuration the
-benchmark uses (default knobs, codebook rows at the recommended stride) and
-checks:
+benchmark uses (kernel 1, 16-document tiles for fp32 and 8 for fp16, codebook
+rows at the recommended stride) and checks:
   * a seeded sample of documents (always including the first and the last)
     against the fp64 oracle under the acceptance rule, and
   * every document's reported distance against the fp64 distance of the
@@ -46,17 +46,17 @@ def _run(cfg_key, batch, cluster, sample, seed, top2=False, f16=False):
     ix = torch.from_numpy(indices).to(dev)
     norms = som.som_codebook_norms(Wd, N=cfg.N)
     perm = som.som_cluster_order(ip, ix, cfg.F) if cluster else None
-    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm)
+    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm, tile_docs=16)
     second = None
     if top2:   # the top-2 search on the same data: same first place, plus the second
-        second = som.som_bmu_search_top2(Wd, norms, ip, ix, N=cfg.N, perm=perm)
+        second = som.som_bmu_search_top2(Wd, norms, ip, ix, N=cfg.N, perm=perm, tile_docs=16)
         assert torch.equal(second[0], bmu) and torch.equal(second[1], dist)
         second = [s.cpu().numpy() for s in second[2:]]
     half = None
     if f16:    # the same codebook stored in fp16 (rounded on the device), searched as such
         W16d = Wd.half()
         n16 = som.som_codebook_norms(W16d, N=cfg.N)
-        half = [x.cpu().numpy() for x in som.som_bmu_search(W16d, n16, ip, ix, N=cfg.N, perm=perm)]
+        half = [x.cpu().numpy() for x in som.som_bmu_search(W16d, n16, ip, ix, N=cfg.N, perm=perm, tile_docs=8)]
         del W16d, n16
     torch.cuda.synchronize()
     bmu, dist = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
