@@ -22,3 +22,9 @@ from .bmu import (  # noqa: F401
     accept_bmu,
     accept_top2,
 )
+from .update import (  # noqa: F401
+    neighbourhood,
+    neighbourhood_radius,
+    update_accumulate,
+    update_finish,
+)
