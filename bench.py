@@ -60,6 +60,9 @@ def parse():
     p.add_argument("--slice-neurons", type=int, default=0)
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage")
     p.add_argument("--top2", action="store_true", help="search the best and second-best unit")
+    p.add_argument("--update", action="store_true",
+                   help="also time the batch-SOM update (accumulate this batch, then the epoch-end blur + write-back)")
+    p.add_argument("--sigma", type=float, default=2.0, help="neighbourhood width of the timed update")
     p.add_argument("--weights", choices=("f32", "f16"), default="f32",
                    help="codebook storage (sums are fp32 either way)")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
@@ -185,6 +188,35 @@ def main():
     st = stage.mean(axis=0)
     log(args, f"step {ms_step:.2f} ms; norms {st[0]:.3f} cluster {st[1]:.3f} plan {st[2]:.3f} search {st[3]:.3f} ms")
 
+    update = None
+    if args.update:
+        side = int(round(N ** 0.5))
+        rows, cols = (side, N // side) if side * (N // side) == N else (1, N)
+        acc = torch.zeros((F, N), dtype=torch.int32, device=dev)
+        cnt = torch.zeros(N, dtype=torch.int32, device=dev)
+        uws = torch.empty(som.som_update_workspace_bytes(F, N), dtype=torch.uint8, device=dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        som.som_update_accumulate(ip, ix, bmu, F, N, acc, cnt)          # warm-up (then reset)
+        acc.zero_()
+        cnt.zero_()
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        som.som_update_accumulate(ip, ix, bmu, F, N, acc, cnt)
+        ev[1].record(stream)
+        som.som_update_finish(Wd, rows, cols, args.sigma, acc, cnt, ws=uws)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        acc_ms, fin_ms = ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
+        wb = 2 if args.weights == "f16" else 4
+        fin_bytes = F * N * (4 + wb)           # algorithmic: accumulators read once, codebook written once
+        update = {"grid": [rows, cols], "sigma": args.sigma, "accumulate_ms": acc_ms, "finish_ms": fin_ms,
+                  "finish_roofline": {"bound": "hbm", "achieved": fin_bytes / (fin_ms * 1e-3) / 1e9,
+                                      "peak": HBM_PEAK_BPS / 1e9, "unit": "GB/s",
+                                      "frac": fin_bytes / (fin_ms * 1e-3) / HBM_PEAK_BPS,
+                                      "algorithmic_bytes": fin_bytes}}
+        log(args, f"update: accumulate {acc_ms:.3f} ms, finish {fin_ms:.3f} ms (sigma {args.sigma})")
+        del acc, cnt, uws
+
     # union sizes of this run's tiles/groups (the plan's per-unit counts)
     ntiles = (B + T - 1) // T
     if kernel == 1:
@@ -281,6 +313,7 @@ def main():
             "alu_useful_adds_frac": useful_adds / search_s / VALU_PEAK_ADDS,
         },
         "cpu_baseline": cpu,
+        "update": update,
         "stages_ms": {"norms": float(st[0]), "cluster": float(st[1]), "plan": float(st[2]),
                       "search": float(st[3])},
         "oracle_check": {"documents": int(len(check)), "rejected": int(bad)},

@@ -268,6 +268,49 @@ som_status som_bmu_search_top2_planned_f16(const uint16_t* W, int64_t F, int64_t
                                            float* dist2, const som_bmu_opts* opts, void* ws,
                                            size_t ws_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Batch-SOM update (the step after the search: the best-matching unit and its
+ * neighbours are updated, Section 3; Section 6.1, Table 4 splits it into a
+ * scatter into accumulators, a neighbourhood blur, a write-back and a norms
+ * refresh).  The paper leaves the neighbourhood function and its schedule to
+ * its companion paper; this library's reading is the textbook batch map:
+ * neuron j sits at row j / cols, column j % cols of a rows x cols grid; the
+ * neighbourhood of width sigma is h(i, j) = exp(-(dr^2 + dc^2) / (2 sigma^2))
+ * for |dr| <= R and |dc| <= R, R = ceil(3 sigma), 0 beyond (sigma = 0: h is
+ * the identity); an epoch's new codebook is
+ *     W[f][j] = sum_i h(i, j) acc[f][i] / sum_i h(i, j) count[i]
+ * wherever the denominator is positive, and unchanged elsewhere.
+ * ------------------------------------------------------------------------- */
+
+/* Accumulate one searched batch: for every document d with bmu[d] in [0, N),
+ * count[bmu[d]] += 1 and acc[f * ld_acc + bmu[d]] += 1 for each of its
+ * features f in [0, F) (other ids are ignored).  uint32 atomics: exact and
+ * independent of order.  The caller zeroes acc [F][ld_acc] and count [N] at
+ * the start of an epoch and calls this once per batch (after the search of
+ * that batch, with its bmu output).  B == 0 is a no-op. */
+som_status som_update_accumulate(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                 const int32_t* bmu, int64_t F, int64_t N, uint32_t* acc, int64_t ld_acc,
+                                 uint32_t* count, hipStream_t stream);
+
+/* End of an epoch: blur the accumulators over the neighbourhood (separable:
+ * a row pass, then a column pass fused with the division) and write the new
+ * weights into W [F][ldw] in place (N = rows * cols <= ldw; rows <= 1024,
+ * cols <= 16384, sigma finite with ceil(3 sigma) <= 4096).  acc and count are
+ * read only.  Sums are fp32 in a fixed tap order (deterministic); the taps
+ * are exp() evaluated in fp64 and rounded to fp32 once.  Refresh the norms
+ * afterwards with som_codebook_norms[_f16].  ws: som_update_workspace_bytes
+ * (F, N) bytes, 256-byte aligned (about 256 MB of it is a chunk of blurred
+ * feature planes; the features are processed in chunks). */
+size_t som_update_workspace_bytes(int64_t F, int64_t N);
+som_status som_update_finish(float* W, int64_t F, int64_t ldw, int32_t rows, int32_t cols, double sigma,
+                             const uint32_t* acc, int64_t ld_acc, const uint32_t* count, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+/* The same for an fp16 codebook (IEEE binary16 bit patterns; the new weights
+ * are rounded to nearest from the fp32 quotient). */
+som_status som_update_finish_f16(uint16_t* W, int64_t F, int64_t ldw, int32_t rows, int32_t cols, double sigma,
+                                 const uint32_t* acc, int64_t ld_acc, const uint32_t* count, void* ws,
+                                 size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,4 +25,7 @@ from .som import (  # noqa: F401
     som_codebook_norms,
     som_last_error,
     som_tile_plan,
+    som_update_accumulate,
+    som_update_finish,
+    som_update_workspace_bytes,
 )

@@ -1,6 +1,7 @@
 // C ABI of libsom (declared in include/som.h): host-side argument checks,
 // workspace carving and kernel sequencing.  No entry point allocates device
 // memory; every array comes from the caller.
+#include <cmath>
 #include <string>
 
 #include "../../include/som.h"
@@ -261,7 +262,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 7; }
+int32_t som_abi_version(void) { return 8; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -548,6 +549,88 @@ som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int6
                                      at<int32_t>(ws, o_iota), at<void>(ws, o_tmp), tb, stream);
   if (e != hipSuccess) return hip_fail(e, "cluster launch");
   return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Batch-SOM update
+// ---------------------------------------------------------------------------
+
+som_status som_update_accumulate(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                 const int32_t* bmu, int64_t F, int64_t N, uint32_t* acc, int64_t ld_acc,
+                                 uint32_t* count, hipStream_t stream) {
+  som_status s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
+  if (N < 1 || N > kI32Max) return fail(SOM_ERR_INVALID_ARG, "N must be in [1, 2^31)");
+  if (ld_acc < N) return fail(SOM_ERR_INVALID_ARG, "ld_acc must be >= N");
+  if (B == 0) return ok();
+  if (!bmu || !acc || !count) return fail(SOM_ERR_INVALID_ARG, "bmu, acc or count is NULL");
+  if (!aligned(acc, 4) || !aligned(count, 4)) return fail(SOM_ERR_INVALID_ARG, "acc and count must be 4-byte aligned");
+  hipError_t e = som::launch_update_accumulate(indptr, indices, B, bmu, F, N, acc, ld_acc, count, stream);
+  if (e != hipSuccess) return hip_fail(e, "accumulate launch");
+  return ok();
+}
+
+static int update_radius(double sigma) { return sigma > 0 ? static_cast<int>(std::ceil(3.0 * sigma)) : 0; }
+
+struct UpdateWs {
+  size_t taps, den_tmp, den, chunk, total;
+  int64_t planes;
+};
+
+static UpdateWs update_ws(int64_t F, int64_t N) {
+  UpdateWs w{};
+  size_t o = 0;
+  w.taps = take(o, sizeof(float) * (som::kUpdateMaxRadius + 1));
+  w.den_tmp = take(o, sizeof(float) * N);
+  w.den = take(o, sizeof(float) * N);
+  w.planes = static_cast<int64_t>(som::update_chunk_planes(F, N));
+  w.chunk = take(o, sizeof(float) * static_cast<size_t>(w.planes) * N);
+  w.total = o;
+  return w;
+}
+
+size_t som_update_workspace_bytes(int64_t F, int64_t N) {
+  if (F < 1 || N < 1 || F > kI32Max || N > kI32Max) return 0;
+  return update_ws(F, N).total;
+}
+
+static som_status finish_impl(void* W, int weights, int64_t F, int64_t ldw, int32_t rows, int32_t cols, double sigma,
+                              const uint32_t* acc, int64_t ld_acc, const uint32_t* count, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  if (!W || !acc || !count) return fail(SOM_ERR_INVALID_ARG, "W, acc or count is NULL");
+  if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
+  if (rows < 1 || cols < 1 || rows > som::kUpdateMaxRows || cols > som::kUpdateMaxCols)
+    return fail(SOM_ERR_INVALID_ARG, "rows must be in [1, 1024] and cols in [1, 16384]");
+  const int64_t N = static_cast<int64_t>(rows) * cols;
+  if (ldw < N || ld_acc < N) return fail(SOM_ERR_INVALID_ARG, "ldw and ld_acc must be >= rows * cols");
+  if (!(sigma >= 0) || !std::isfinite(sigma)) return fail(SOM_ERR_INVALID_ARG, "sigma must be finite and >= 0");
+  const int R = sigma * 3.0 > som::kUpdateMaxRadius ? som::kUpdateMaxRadius + 1 : update_radius(sigma);
+  if (R > som::kUpdateMaxRadius) return fail(SOM_ERR_INVALID_ARG, "sigma too large: ceil(3 sigma) must be <= 4096");
+  if (!aligned(W, weights == som::kWeightsF16 ? 2 : 4) || !aligned(acc, 4) || !aligned(count, 4))
+    return fail(SOM_ERR_INVALID_ARG, "W, acc or count misaligned");
+  const UpdateWs w = update_ws(F, N);
+  if (!ws) return fail(SOM_ERR_WORKSPACE, "ws is NULL");
+  if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
+  if (ws_bytes < w.total)
+    return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(w.total) + " bytes");
+  hipError_t e = som::launch_update_finish(W, weights, F, ldw, rows, cols, sigma, R, acc, ld_acc, count,
+                                           at<float>(ws, w.taps), at<float>(ws, w.den_tmp), at<float>(ws, w.den),
+                                           at<float>(ws, w.chunk), w.planes, stream);
+  if (e != hipSuccess) return hip_fail(e, "update launch");
+  return ok();
+}
+
+som_status som_update_finish(float* W, int64_t F, int64_t ldw, int32_t rows, int32_t cols, double sigma,
+                             const uint32_t* acc, int64_t ld_acc, const uint32_t* count, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  return finish_impl(W, som::kWeightsF32, F, ldw, rows, cols, sigma, acc, ld_acc, count, ws, ws_bytes, stream);
+}
+
+som_status som_update_finish_f16(uint16_t* W, int64_t F, int64_t ldw, int32_t rows, int32_t cols, double sigma,
+                                 const uint32_t* acc, int64_t ld_acc, const uint32_t* count, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  return finish_impl(W, som::kWeightsF16, F, ldw, rows, cols, sigma, acc, ld_acc, count, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

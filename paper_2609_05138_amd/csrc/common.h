@@ -99,6 +99,19 @@ hipError_t launch_search_k1_f16(const SearchArgs& a, hipStream_t stream);
 // keys into results in input order.
 hipError_t launch_merge(const SearchArgs& a, hipStream_t stream);
 
+// Batch-SOM update (update.hip).
+constexpr int kUpdateMaxRows = 1024;   // column-blur strip: rows x 32 fp32 in LDS
+constexpr int kUpdateMaxCols = 16384;  // row blur: one grid row in LDS
+constexpr int kUpdateMaxRadius = 4096;
+size_t update_chunk_planes(int64_t F, int64_t N);
+hipError_t launch_update_accumulate(const int32_t* indptr, const int32_t* indices, int64_t B, const int32_t* bmu,
+                                    int64_t F, int64_t N, uint32_t* acc, int64_t ld_acc, uint32_t* count,
+                                    hipStream_t stream);
+hipError_t launch_update_finish(void* W, int weights, int64_t F, int64_t ldw, int rows, int cols, double sigma, int R,
+                                const uint32_t* acc, int64_t ld_acc, const uint32_t* count, float* taps,
+                                float* den_tmp, float* den, float* chunk, int64_t chunk_planes,
+                                hipStream_t stream);
+
 // Clustering.
 size_t cluster_sort_temp_bytes(int64_t B, int64_t F);
 hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,

@@ -44,6 +44,10 @@ EXPORTS = (
     "som_bmu_search_top2_f16",
     "som_bmu_search_planned_f16",
     "som_bmu_search_top2_planned_f16",
+    "som_update_accumulate",
+    "som_update_workspace_bytes",
+    "som_update_finish",
+    "som_update_finish_f16",
 )
 
 
@@ -124,6 +128,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         fn = getattr(lib, base + "_f16")
         fn.restype = _i32
         fn.argtypes = getattr(lib, base).argtypes
+    lib.som_update_accumulate.restype = _i32
+    lib.som_update_accumulate.argtypes = [_vp, _vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _vp]
+    lib.som_update_workspace_bytes.restype = _sz
+    lib.som_update_workspace_bytes.argtypes = [_i64, _i64]
+    for fn in (lib.som_update_finish, lib.som_update_finish_f16):
+        fn.restype = _i32
+        fn.argtypes = [_vp, _i64, _i64, _i32, _i32, ctypes.c_double, _vp, _i64, _vp, _vp, _sz, _vp]
     lib.som_cluster_order.restype = _i32
     lib.som_cluster_order.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _sz, _vp]
     _lib = lib
@@ -419,3 +430,39 @@ def som_cluster_order(indptr: torch.Tensor, indices: torch.Tensor, F: int,
     _check(lib.som_cluster_order(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), _ptr(ws), ws.numel(),
                                  _stream(stream)))
     return perm[:B]
+
+
+def som_update_accumulate(indptr: torch.Tensor, indices: torch.Tensor, bmu: torch.Tensor, F: int, N: int,
+                          acc: torch.Tensor, count: torch.Tensor, stream=None) -> None:
+    """acc [F, ld_acc] and count [N] (int32 tensors holding uint32 counts) += one searched batch."""
+    lib = load()
+    for t, name in ((indptr, "indptr"), (indices, "indices"), (bmu, "bmu"), (acc, "acc"), (count, "count")):
+        _dev(t, torch.int32, name)
+    B = indptr.numel() - 1
+    if acc.dim() != 2 or acc.shape[0] != F or acc.shape[1] < N or count.numel() < N or bmu.numel() < B:
+        raise ValueError("acc must be [F, >= N], count [>= N], bmu [>= B]")
+    _check(lib.som_update_accumulate(_ptr(indptr), _ptr(indices), B, indices.numel(), _ptr(bmu), F, N, _ptr(acc),
+                                     acc.shape[1], _ptr(count), _stream(stream)))
+
+
+def som_update_workspace_bytes(F: int, N: int) -> int:
+    return int(load().som_update_workspace_bytes(F, N))
+
+
+def som_update_finish(W: torch.Tensor, rows: int, cols: int, sigma: float, acc: torch.Tensor, count: torch.Tensor,
+                      ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Blur the accumulators over the neighbourhood and write the new weights into W (fp32 or fp16)."""
+    lib = load()
+    sfx = _codebook(W)
+    _dev(acc, torch.int32, "acc")
+    _dev(count, torch.int32, "count")
+    F, ldw = W.shape
+    if acc.dim() != 2 or acc.shape[0] != F:
+        raise ValueError("acc must be [F, ld_acc]")
+    if ws is None:
+        ws = _workspace(lib.som_update_workspace_bytes(F, rows * cols), W.device)
+    _dev(ws, torch.uint8, "ws")
+    _check(getattr(lib, "som_update_finish" + sfx)(_ptr(W), F, ldw, rows, cols, float(sigma), _ptr(acc),
+                                                   acc.shape[1], _ptr(count), _ptr(ws), ws.numel(),
+                                                   _stream(stream)))
+

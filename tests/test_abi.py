@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 7
+    assert som.som_abi_version() == 8
 
 
 def test_codebook_ldw_is_host_only(lib):
@@ -183,6 +183,31 @@ def test_f16_rejects_bad_arguments(lib):
     assert st == som.SOM_ERR_INVALID_ARG and "multiple of 8" in msg
     st, _ = _status(lib, "som_codebook_norms_f16", null, 8, 8, 8, fake, null)
     assert st == som.SOM_ERR_INVALID_ARG
+
+
+def test_update_rejects_bad_arguments(lib):
+    null = None
+    fake = ctypes.c_void_p(0x1000)
+    # indptr, indices, B, nnz, bmu, F, N, acc, ld_acc, count, stream
+    assert _status(lib, "som_update_accumulate", fake, fake, 4, 10, fake, 8, 16, fake, 15, fake, null)[0] \
+        == som.SOM_ERR_INVALID_ARG                                          # ld_acc < N
+    assert _status(lib, "som_update_accumulate", fake, fake, 4, 10, null, 8, 16, fake, 16, fake, null)[0] \
+        == som.SOM_ERR_INVALID_ARG
+    assert _status(lib, "som_update_accumulate", null, null, 0, 0, null, 8, 16, null, 16, null, null)[0] == som.SOM_OK
+    ws = lib.som_update_workspace_bytes(20000, 262144)
+    assert ws >= 4 * ((1 << 26) + 2 * 262144) and ws % 256 == 0
+    assert lib.som_update_workspace_bytes(0, 10) == 0
+
+    def fin(rows=4, cols=4, sigma=1.0, ldw=16, ld_acc=16, ws=fake, ws_bytes=1 << 40, W=fake):
+        return _status(lib, "som_update_finish", W, 8, ldw, rows, cols, sigma, fake, ld_acc, fake, ws, ws_bytes, null)
+
+    for kw in (dict(rows=0), dict(cols=0), dict(rows=1025), dict(cols=16385), dict(sigma=-1.0),
+               dict(sigma=float("nan")), dict(sigma=float("inf")), dict(sigma=2000.0), dict(ldw=15),
+               dict(ld_acc=15), dict(W=null)):
+        st, msg = fin(**kw)
+        assert st == som.SOM_ERR_INVALID_ARG, (kw, msg)
+    assert fin(ws=null)[0] == som.SOM_ERR_WORKSPACE
+    assert fin(ws_bytes=64)[0] == som.SOM_ERR_WORKSPACE
 
 
 def test_plan_and_cluster_reject_bad_arguments(lib):
