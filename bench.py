@@ -60,6 +60,9 @@ def parse():
     p.add_argument("--slice-neurons", type=int, default=0)
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage")
     p.add_argument("--top2", action="store_true", help="search the best and second-best unit")
+    p.add_argument("--unfused", action="store_true",
+                   help="time the unfused comparator (distance block + separate argmin) instead of the fused search")
+    p.add_argument("--block-docs", type=int, default=8192, help="documents per distance block (--unfused)")
     p.add_argument("--update", action="store_true",
                    help="also time the batch-SOM update (accumulate this batch, then the epoch-end blur + write-back)")
     p.add_argument("--sigma", type=float, default=2.0, help="neighbourhood width of the timed update")
@@ -147,6 +150,12 @@ def main():
                        dtype=torch.uint8, device=dev)
     plan_buf = torch.empty(max(som.load().som_plan_bytes(B, nnz, ctypes.byref(som.som._opts(**knobs))), 1),
                            dtype=torch.uint8, device=dev)
+    u_ws = None
+    if args.unfused:
+        if args.weights != "f32" or args.top2 or kernel != 1:
+            raise SystemExit("--unfused runs the fp32, kernel-1, best-unit search only")
+        u_ws = torch.empty(som.som_bmu_search_unfused_workspace_bytes(F, N, B, nnz, args.block_docs, **knobs),
+                           dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -159,6 +168,14 @@ def main():
             som.som_cluster_order(ip, ix, F, perm=perm, ws=cl_ws)
         if ev:
             ev[2].record(stream)
+        if args.unfused:   # the comparator plans inside its own call: its plan stage is in "search"
+            if ev:
+                ev[3].record(stream)
+            som.som_bmu_search_unfused(Wd, norms, ip, ix, N=N, perm=perm, block_docs=args.block_docs, bmu=bmu,
+                                       dist=dist, ws=u_ws, **knobs)
+            if ev:
+                ev[4].record(stream)
+            return None
         plan = som.som_plan(ip, ix, F, perm=perm, plan=plan_buf, **knobs)
         if ev:
             ev[3].record(stream)
@@ -224,7 +241,7 @@ def main():
     else:
         cnt = som.som_group_plan(ip, ix, F, T, perm=perm)[1]
     union_total = int(cnt.to(torch.int64).sum().item())
-    measured = None if args.top2 else MEASURED_TRAFFIC.get(
+    measured = None if (args.top2 or args.unfused) else MEASURED_TRAFFIC.get(
         (cfg.name, args.batch, B, ldw, args.weights, kernel, json.dumps(knobs, sort_keys=True)))
     pairs = B * N
     value = pairs / (ms_step * 1e-3)
@@ -233,6 +250,8 @@ def main():
     # once per tile (kernel 1) or group (kernel 2), plus the fp32 norms once per unit
     wbytes = 2.0 if args.weights == "f16" else 4.0
     l2_bytes = N * (wbytes * union_total + 4.0 * ntiles)
+    if args.unfused:   # the distance block is written once and read back once
+        l2_bytes += 8.0 * B * N
     useful_adds = float(nnz) * N
 
     # spot check of this run's results against the oracle
@@ -296,10 +315,13 @@ def main():
             "N": N, "F": F, "ldw": ldw, "B": B, "nnz": nnz, "docs_per_union_sweep": T,
             "knobs": {k: (v or "auto") for k, v in knobs.items()}, "clustered": perm is not None,
             "second_best_unit": bool(args.top2), "weights": args.weights,
+            "unfused_block_docs": args.block_docs if args.unfused else None,
+            "score_block_bytes": 4 * args.block_docs * N if args.unfused else 0,
             "bmu_pass_ms": float(st[1] + st[2] + st[3]),
         },
         "roofline": {
-            "kernel": ("k_search_docs" if kernel == 2 else "k_search") + " (fused union sweep + argmin) with key init and decode",
+            "kernel": ("k_search (union sweep writing the distance block) + k_argmin_rows" if args.unfused else
+                       ("k_search_docs" if kernel == 2 else "k_search") + " (fused union sweep + argmin) with key init and decode"),
             "bound": "l2",
             "achieved": l2_bytes / search_s / 1e9,
             "peak": L2_PEAK_BPS / 1e9,

@@ -268,6 +268,24 @@ som_status som_bmu_search_top2_planned_f16(const uint16_t* W, int64_t F, int64_t
                                            float* dist2, const som_bmu_opts* opts, void* ws,
                                            size_t ws_bytes, hipStream_t stream);
 
+/* Unfused comparator (an ablation, not the method): the same search with the
+ * argmin NOT fused into the product, the design the paper's fused kernel is
+ * measured against (Section 3: the comparison computes the sparse-dense
+ * product, materialises the score block, then reduces it with a separate
+ * argmin pass; Section 4.4).  Kernel 1's union sweep writes the distance block
+ * of block_docs documents at a time (fp32 [block_docs][N], in ws), then one
+ * wave per document reduces its row.  The distances are the fused search's
+ * fp32 values, so bmu and dist are bit-identical to som_bmu_search's with the
+ * same opts.  Kernel 1 and an fp32 codebook only; block_docs a positive
+ * multiple of the tile size.  ws: som_bmu_search_unfused_workspace_bytes
+ * (plan + score block). */
+size_t som_bmu_search_unfused_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
+                                              const som_bmu_opts* opts, int64_t block_docs);
+som_status som_bmu_search_unfused(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                                  const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                  const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                                  int64_t block_docs, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Batch-SOM update (the step after the search: the best-matching unit and its
  * neighbours are updated, Section 3; Section 6.1, Table 4 splits it into a

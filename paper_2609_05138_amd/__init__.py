@@ -15,6 +15,8 @@ from .som import (  # noqa: F401
     som_bmu_search_planned,
     som_bmu_search_top2,
     som_bmu_search_top2_planned,
+    som_bmu_search_unfused,
+    som_bmu_search_unfused_workspace_bytes,
     som_bmu_search_planned_workspace_bytes,
     som_bmu_workspace_bytes,
     som_group_plan,

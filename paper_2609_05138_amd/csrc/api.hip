@@ -232,6 +232,8 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
   a.slice = p.NB;
   a.ntiles = p.nunits;
   a.nchunks = p.nchunks;
+  a.tile_base = 0;
+  a.tile_end = p.nunits;
   if (p.kernel == 1) {
     a.tile_offset = at<int32_t>(plan, l.offset);
     a.tile_count = at<int32_t>(plan, l.count);
@@ -262,7 +264,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 8; }
+int32_t som_abi_version(void) { return 9; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -548,6 +550,93 @@ som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int6
                                      at<uint64_t>(ws, o_keys), at<uint64_t>(ws, o_sorted),
                                      at<int32_t>(ws, o_iota), at<void>(ws, o_tmp), tb, stream);
   if (e != hipSuccess) return hip_fail(e, "cluster launch");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Unfused comparator
+// ---------------------------------------------------------------------------
+
+struct UnfusedWs {
+  PlanLayout plan;
+  size_t score, total;
+};
+
+static UnfusedWs unfused_ws(const Plan& p, int64_t N, int64_t nnz, int64_t block_docs) {
+  UnfusedWs w{};
+  w.plan = plan_layout(p, nnz);
+  size_t o = w.plan.total;
+  w.score = take(o, sizeof(float) * static_cast<size_t>(block_docs) * static_cast<size_t>(N));
+  w.total = o;
+  return w;
+}
+
+static som_status unfused_plan(int64_t N, int64_t B, const som_bmu_opts* opts, int64_t block_docs, Plan* p) {
+  som_status s = make_plan(N, B, opts, p);
+  if (s != SOM_OK) return s;
+  if (p->kernel != 1) return fail(SOM_ERR_INVALID_ARG, "the unfused comparator uses kernel 1");
+  if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on the unfused comparator");
+  if (block_docs < p->T || block_docs % p->T != 0)
+    return fail(SOM_ERR_INVALID_ARG, "block_docs must be a positive multiple of the tile size");
+  if (block_docs > (int64_t(1) << 40) / N) return fail(SOM_ERR_INVALID_ARG, "block_docs * N too large");
+  return SOM_OK;
+}
+
+size_t som_bmu_search_unfused_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
+                                              const som_bmu_opts* opts, int64_t block_docs) {
+  if (F < 1 || N < 1 || B < 0 || nnz < 0) return 0;
+  Plan p;
+  if (unfused_plan(N, B, opts, block_docs, &p) != SOM_OK) return 0;
+  return unfused_ws(p, N, nnz, block_docs).total;
+}
+
+som_status som_bmu_search_unfused(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                                  const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                  const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                                  int64_t block_docs, void* ws, size_t ws_bytes, hipStream_t stream) {
+  som_status s = check_codebook(W, som::kWeightsF32, F, N, ldw);
+  if (s != SOM_OK) return s;
+  if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
+  s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (B > 0 && (!bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "bmu or dist is NULL");
+  Plan p;
+  s = unfused_plan(N, B, opts, block_docs, &p);
+  if (s != SOM_OK) return s;
+  const UnfusedWs w = unfused_ws(p, N, nnz, block_docs);
+  if (B == 0) return ok();
+  if (!ws) return fail(SOM_ERR_WORKSPACE, "ws is NULL");
+  if (!aligned(ws, 256)) return fail(SOM_ERR_INVALID_ARG, "ws must be 256-byte aligned");
+  if (ws_bytes < w.total)
+    return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(w.total) + " bytes");
+  hipError_t e = build_plan(indptr, indices, B, F, perm, p, ws, w.plan, stream);
+  if (e != hipSuccess) return hip_fail(e, "plan launch");
+  som::SearchArgs a{};
+  a.W = W;
+  a.weights = som::kWeightsF32;
+  a.F = F;
+  a.N = N;
+  a.ldw = ldw;
+  a.norms = norms;
+  a.indptr = indptr;
+  a.perm = perm;
+  a.B = B;
+  a.kernel = 1;
+  a.T = p.T;
+  a.K = p.K;
+  a.group = p.group;
+  a.mask_mode = p.mask_mode;
+  a.ntiles = p.nunits;
+  a.nchunks = p.nchunks;
+  a.tile_offset = at<int32_t>(ws, w.plan.offset);
+  a.tile_count = at<int32_t>(ws, w.plan.count);
+  a.union_feat = at<int32_t>(ws, w.plan.feat);
+  a.union_mask = at<uint32_t>(ws, w.plan.extra);
+  a.score = at<float>(ws, w.score);
+  a.bmu = bmu;
+  a.dist = dist;
+  e = som::launch_unfused(a, block_docs, stream);
+  if (e != hipSuccess) return hip_fail(e, "unfused launch");
   return ok();
 }
 

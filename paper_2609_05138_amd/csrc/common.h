@@ -73,6 +73,10 @@ struct SearchArgs {
   int mask_mode;    // 0 = branch-free fma by the membership bit, 1 = scalar branches
   int64_t ntiles;
   int64_t nchunks;  // neuron slices = ceil(N / (64 * K))
+  int64_t tile_base = 0;  // kernel 1 searches tiles [tile_base, tile_end) of the plan
+  int64_t tile_end = 0;
+  float* score = nullptr;  // unfused comparator: distances of tiled-order documents
+                           // [tile_base * T, ...) go to score[(p - tile_base * T) * N + j]
   const int32_t* tile_offset;
   const int32_t* tile_count;
   const int32_t* union_feat;
@@ -95,6 +99,9 @@ struct SearchArgs {
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream);
 // Kernel 1 over an fp16 codebook (its own translation unit).
 hipError_t launch_search_k1_f16(const SearchArgs& a, hipStream_t stream);
+// Unfused comparator: kernel 1 writes the distance block of block_docs
+// documents at a time into `score`, then a wave-per-row argmin reduces it.
+hipError_t launch_unfused(SearchArgs a, int64_t block_docs, hipStream_t stream);
 // Initialises the keys, then runs the fused search; launch_merge decodes the
 // keys into results in input order.
 hipError_t launch_merge(const SearchArgs& a, hipStream_t stream);

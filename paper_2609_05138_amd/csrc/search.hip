@@ -178,6 +178,51 @@ __global__ void __launch_bounds__(256) k_decode(SearchArgs a) {
   }
 }
 
+// Unfused comparator, second pass: one wave per row of the distance block
+// (one document), lanes striding the row with 128-bit loads; each lane keeps
+// its first minimum in ascending j, then the wave reduces packed keys, so the
+// lowest index wins ties exactly as in the fused search.
+__global__ void __launch_bounds__(256)
+k_argmin_rows(const float* __restrict__ score, int64_t N, int64_t p0, int64_t rows, const int32_t* __restrict__ perm,
+              int32_t* __restrict__ bmu, float* __restrict__ dist) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const float* row = score + r * N;
+  float best = 0.f;
+  uint32_t bj = 0xffffffffu;
+  const int64_t n4 = N / 4 * 4;
+  for (int64_t j = 4 * lane; j < n4; j += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(row + j);
+    const float x[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (bj == 0xffffffffu || x[e] < best) {
+        best = x[e];
+        bj = static_cast<uint32_t>(j + e);
+      }
+  }
+  for (int64_t j = n4 + lane; j < N; j += 64)
+    if (bj == 0xffffffffu || row[j] < best) {
+      best = row[j];
+      bj = static_cast<uint32_t>(j);
+    }
+  uint64_t key = bj == 0xffffffffu ? kNoKey : pack_key(best, bj);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(key), off, 64);
+    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(key >> 32), off, 64);
+    const uint64_t o = (static_cast<uint64_t>(hi) << 32) | lo;
+    key = o < key ? o : key;
+  }
+  if (lane == 0) {
+    const int64_t p = p0 + r;
+    const int64_t d = perm ? static_cast<int64_t>(perm[p]) : p;
+    bmu[d] = static_cast<int32_t>(static_cast<uint32_t>(key));
+    dist[d] = from_ordered_bits(static_cast<uint32_t>(key >> 32));
+  }
+}
+
 template <int NB, int G>
 hipError_t launch_docs_ng(const SearchArgs& a, hipStream_t stream) {
   const int64_t ngroups = (a.B + 64 * G - 1) / (64 * G);
@@ -208,10 +253,7 @@ hipError_t launch_docs(const SearchArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(k_keys_init, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream,
-                     a.keys, a.keys2, a.B);
-  if (a.kernel == 2) return launch_docs(a, stream);
+hipError_t launch_k1(const SearchArgs& a, hipStream_t stream) {
   if (a.weights == kWeightsF16) return launch_search_k1_f16(a, stream);
   switch (a.T) {
     case 1: return a.K == 4 ? launch_tk<float, 1, 4>(a, stream) : launch_tk<float, 1, 8>(a, stream);
@@ -222,6 +264,30 @@ hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {
     case 32: return launch_tk<float, 32, 4>(a, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(k_keys_init, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream,
+                     a.keys, a.keys2, a.B);
+  if (a.kernel == 2) return launch_docs(a, stream);
+  return launch_k1(a, stream);
+}
+
+hipError_t launch_unfused(SearchArgs a, int64_t block_docs, hipStream_t stream) {
+  const int64_t tiles_per_block = block_docs / a.T;
+  for (int64_t t0 = 0; t0 < a.ntiles; t0 += tiles_per_block) {
+    a.tile_base = t0;
+    a.tile_end = t0 + tiles_per_block < a.ntiles ? t0 + tiles_per_block : a.ntiles;
+    hipError_t e = launch_k1(a, stream);
+    if (e != hipSuccess) return e;
+    const int64_t p0 = t0 * a.T;
+    const int64_t rows = (a.tile_end * a.T < a.B ? a.tile_end * a.T : a.B) - p0;
+    hipLaunchKernelGGL(k_argmin_rows, dim3(static_cast<uint32_t>((rows + 3) / 4)), dim3(256), 0, stream, a.score,
+                       a.N, p0, rows, a.perm, a.bmu, a.dist);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_merge(const SearchArgs& a, hipStream_t stream) {

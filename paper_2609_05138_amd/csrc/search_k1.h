@@ -191,9 +191,9 @@ k_search(SearchArgs a) {
   // tiled order, which share features, share that XCD's L2.
   const uint32_t per_xcd = gridDim.x / kXcds;
   const uint32_t wg = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  const int64_t t = static_cast<int64_t>(wg) * G + wave;         // this wave's tile
-  const int64_t c = blockIdx.y;                                  // neuron slice
-  if (t >= a.ntiles) return;                                     // no barriers below
+  const int64_t t = a.tile_base + static_cast<int64_t>(wg) * G + wave;  // this wave's tile
+  const int64_t c = blockIdx.y;                                         // neuron slice
+  if (t >= a.tile_end) return;                                          // no barriers below
   int2* ent = ent_all[wave];
   if (lane < 2 * U) ent[kEntryChunk + lane] = make_int2(0, 0);
 
@@ -280,6 +280,17 @@ k_search(SearchArgs a) {
     if (p >= a.B) break;
     const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
     const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
+    if (a.score) {  // unfused comparator: write the distances, no argmin here
+      float* row = a.score + (p - a.tile_base * T) * a.N;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int64_t j = n0 + 64 * E * q + E * lane + e;
+          if (j < a.N) row[j] = fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]);
+        }
+      continue;
+    }
     if (a.keys2) {  // best and second best (wave-uniform branch)
       uint64_t k1 = kNoKey, k2 = kNoKey;
 #pragma unroll
@@ -326,7 +337,7 @@ hipError_t launch_tkg(const SearchArgs& a, hipStream_t stream) {
   constexpr int Q = K / Storage<WT>::kE;
   constexpr int U = Q == 1 ? (sizeof(WT) == 2 ? (T >= 16 ? 2 : 4) : (T >= 16 ? 4 : 8)) : 4;
   // tile groups rounded up to a multiple of the XCD count (see k_search)
-  const int64_t groups = (a.ntiles + G - 1) / G;
+  const int64_t groups = (a.tile_end - a.tile_base + G - 1) / G;
   const dim3 grid(static_cast<uint32_t>((groups + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));
   if (a.mask_mode == kMaskBranch)
     hipLaunchKernelGGL((k_search<WT, T, K, G, U, kMaskBranch>), grid, dim3(G * 64), 0, stream, a);

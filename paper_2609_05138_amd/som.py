@@ -44,6 +44,8 @@ EXPORTS = (
     "som_bmu_search_top2_f16",
     "som_bmu_search_planned_f16",
     "som_bmu_search_top2_planned_f16",
+    "som_bmu_search_unfused_workspace_bytes",
+    "som_bmu_search_unfused",
     "som_update_accumulate",
     "som_update_workspace_bytes",
     "som_update_finish",
@@ -128,6 +130,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         fn = getattr(lib, base + "_f16")
         fn.restype = _i32
         fn.argtypes = getattr(lib, base).argtypes
+    lib.som_bmu_search_unfused_workspace_bytes.restype = _sz
+    lib.som_bmu_search_unfused_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, ctypes.POINTER(som_bmu_opts), _i64]
+    lib.som_bmu_search_unfused.restype = _i32
+    lib.som_bmu_search_unfused.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp,
+                                           ctypes.POINTER(som_bmu_opts), _i64, _vp, _sz, _vp]
     lib.som_update_accumulate.restype = _i32
     lib.som_update_accumulate.argtypes = [_vp, _vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _vp]
     lib.som_update_workspace_bytes.restype = _sz
@@ -465,4 +472,38 @@ def som_update_finish(W: torch.Tensor, rows: int, cols: int, sigma: float, acc: 
     _check(getattr(lib, "som_update_finish" + sfx)(_ptr(W), F, ldw, rows, cols, float(sigma), _ptr(acc),
                                                    acc.shape[1], _ptr(count), _ptr(ws), ws.numel(),
                                                    _stream(stream)))
+
+
+def som_bmu_search_unfused_workspace_bytes(F: int, N: int, B: int, nnz: int, block_docs: int, **knobs) -> int:
+    o = _opts(**knobs)
+    return int(load().som_bmu_search_unfused_workspace_bytes(F, N, B, nnz, ctypes.byref(o), int(block_docs)))
+
+
+def som_bmu_search_unfused(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, indices: torch.Tensor,
+                           N: Optional[int] = None, perm: Optional[torch.Tensor] = None, block_docs: int = 8192,
+                           bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None,
+                           ws: Optional[torch.Tensor] = None, stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
+    """The search with a materialised score block (the unfused comparator):
+    same (bmu, dist) as som_bmu_search, bit for bit."""
+    lib = load()
+    _dev(W, torch.float32, "W")
+    _dev(norms, torch.float32, "norms")
+    _dev(indptr, torch.int32, "indptr")
+    _dev(indices, torch.int32, "indices")
+    F, ldw = W.shape
+    n = ldw if N is None else int(N)
+    B = indptr.numel() - 1
+    nnz = indices.numel()
+    if perm is not None:
+        _dev(perm, torch.int32, "perm")
+    bmu, dist = _outputs(B, W.device, [(bmu, torch.int32, "bmu"), (dist, torch.float32, "dist")])
+    o = _opts(**knobs)
+    if ws is None:
+        ws = _workspace(lib.som_bmu_search_unfused_workspace_bytes(F, n, B, nnz, ctypes.byref(o), int(block_docs)),
+                        W.device)
+    _dev(ws, torch.uint8, "ws")
+    _check(lib.som_bmu_search_unfused(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), _ptr(indices), B, nnz,
+                                      _ptr(perm), _ptr(bmu), _ptr(dist), ctypes.byref(o), int(block_docs), _ptr(ws),
+                                      ws.numel(), _stream(stream)))
+    return bmu, dist
 

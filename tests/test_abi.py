@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 8
+    assert som.som_abi_version() == 9
 
 
 def test_codebook_ldw_is_host_only(lib):
@@ -208,6 +208,26 @@ def test_update_rejects_bad_arguments(lib):
         assert st == som.SOM_ERR_INVALID_ARG, (kw, msg)
     assert fin(ws=null)[0] == som.SOM_ERR_WORKSPACE
     assert fin(ws_bytes=64)[0] == som.SOM_ERR_WORKSPACE
+
+
+def test_unfused_rejects_bad_arguments(lib):
+    null = None
+    fake = ctypes.c_void_p(0x1000)
+    O = som.som_bmu_opts
+
+    def call(opts=None, block=64, ws_bytes=1 << 40):
+        o = opts if opts is not None else O()
+        return _status(lib, "som_bmu_search_unfused", fake, 8, 8, 8, fake, fake, fake, 4, 10, null, fake, fake,
+                       ctypes.byref(o), block, fake, ws_bytes, null)
+
+    for bad in (dict(opts=O(2)), dict(block=0), dict(block=12), dict(block=-8)):
+        st, msg = call(**bad)
+        assert st == som.SOM_ERR_INVALID_ARG, (bad, msg)
+    assert call(ws_bytes=64)[0] == som.SOM_ERR_WORKSPACE
+    o = O()
+    need = lib.som_bmu_search_unfused_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o), 8192)
+    assert need >= 4 * 8192 * 262144
+    assert lib.som_bmu_search_unfused_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o), 12) == 0
 
 
 def test_plan_and_cluster_reject_bad_arguments(lib):

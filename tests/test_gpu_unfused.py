@@ -1,0 +1,101 @@
+"""GPU parity of the unfused comparator (distance block + separate argmin)
+through the C ABI.  Its distances are the fused search's fp32 values, so the
+outputs must equal the fused search's bit for bit, for any block size, tile
+size, lane width and tile order; the fused search itself is checked against
+the oracle elsewhere, and the hand-worked examples pin it directly here."""
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import GOLDEN
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2609_05138_amd as som
+else:  # collected on CPU-only machines, never run there
+    som = None
+
+DEV = "cuda:0"
+
+
+def _i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(DEV)
+
+
+def _dev_W(W, ldw=None):
+    F, N = W.shape
+    ld = ((N + 3) // 4 * 4) if ldw is None else ldw
+    Wp = np.zeros((F, ld), np.float32)
+    Wp[:, :N] = W
+    return torch.from_numpy(Wp).to(DEV)
+
+
+def _both(W, indptr, indices, block_docs, perm=None, ldw=None, **knobs):
+    Wd = _dev_W(W, ldw)
+    N = W.shape[1]
+    norms = som.som_codebook_norms(Wd, N=N)
+    ip, ix = _i32(indptr), _i32(indices)
+    p = None if perm is None else _i32(perm)
+    fused = som.som_bmu_search(Wd, norms, ip, ix, N=N, perm=p, **knobs)
+    unf = som.som_bmu_search_unfused(Wd, norms, ip, ix, N=N, perm=p, block_docs=block_docs, **knobs)
+    torch.cuda.synchronize()
+    return [t.cpu().numpy() for t in fused], [t.cpu().numpy() for t in unf]
+
+
+def test_unfused_hand_examples_exact():
+    for ex in json.load(open(os.path.join(GOLDEN, "hand_examples.json")))["examples"]:
+        F, N = ex["F"], ex["N"]
+        W = np.zeros((F, N), np.float32)
+        for j, w in enumerate(ex["neurons"]):
+            for f, v in enumerate(w):
+                W[f, j] = float(Fraction(v))
+        docs = [d["features"] for d in ex["docs"]]
+        indptr = np.concatenate([[0], np.cumsum([len(d) for d in docs])])
+        indices = np.array([f for d in docs for f in d], dtype=np.int64)
+        for T, block in ((1, 1), (1, 3), (8, 8), (8, 16)):
+            _, (bmu, dist) = _both(W, indptr, indices, block, tile_docs=T)
+            assert bmu.tolist() == [d["bmu"] for d in ex["docs"]]
+            assert dist.tolist() == [float(Fraction(d["d"][d["bmu"]])) for d in ex["docs"]]
+
+
+def test_unfused_equals_fused_config1_every_document():
+    from synth import codebook, documents
+    W = codebook(1)
+    indptr, indices = documents(1, 0)
+    for block in (8, 64, 1000, 16384):
+        f, u = _both(W, indptr, indices, block)
+        assert np.array_equal(f[0], u[0]) and np.array_equal(f[1], u[1]), block
+
+
+@pytest.mark.parametrize("knobs,block", [(dict(), 8), (dict(), 200), (dict(tile_docs=16), 48),
+                                         (dict(tile_docs=1, lane_neurons=8), 37),
+                                         (dict(tile_docs=32), 4096), (dict(group_tiles=4, mask_mode=1), 512)])
+def test_unfused_equals_fused_ragged_map(knobs, block):
+    from synth import codebook, documents
+    W = codebook(2, N=4101, F=20000)                  # N not a multiple of 4: the argmin tail path
+    indptr, indices = documents(2, 0, n_docs=3001)
+    perm = np.random.default_rng(7).permutation(3001)
+    for p in (None, perm, oracle.cluster_order(indptr, indices, 20000)):
+        f, u = _both(W, indptr, indices, block, perm=p, ldw=4104, **knobs)
+        assert np.array_equal(f[0], u[0]) and np.array_equal(f[1], u[1]), (knobs, block)
+
+
+def test_unfused_equals_fused_on_the_512_map():
+    from synth import CONFIGS, codebook, documents
+    cfg = CONFIGS[4]                                   # the 21 GB codebook is not needed: 4000 of its rows
+    Wsub = codebook(cfg, F=4000)                       # 4000 features x 262,144 neurons
+    indptr, indices = documents(cfg, 0, n_docs=4096)
+    keep = indices < 4000                              # documents restricted to those features
+    counts = np.add.reduceat(keep.astype(np.int64), indptr[:-1]) if len(indices) else np.zeros(4096, np.int64)
+    counts[np.diff(indptr) == 0] = 0
+    indptr2 = np.concatenate([[0], np.cumsum(counts)])
+    indices2 = indices[keep]
+    f, u = _both(Wsub, indptr2, indices2, 2048, ldw=som.som_codebook_ldw(cfg.N), tile_docs=16)
+    assert np.array_equal(f[0], u[0]) and np.array_equal(f[1], u[1])
