@@ -52,8 +52,10 @@ def parse():
     p.add_argument("--batch", type=int, default=0)
     p.add_argument("--docs", type=int, default=0, help="override documents per batch (0 = config)")
     p.add_argument("--ldw", type=int, default=0, help="codebook row stride in floats (0 = recommended)")
-    p.add_argument("--kernel", type=int, default=0, help="0 auto, 1 neurons on lanes, 2 documents on lanes")
-    p.add_argument("--tile-docs", type=int, default=0, help="0: 16 for fp32, 8 for fp16 codebooks")
+    p.add_argument("--kernel", type=int, default=0,
+                   help="0 auto, 1 neurons on lanes, 2 documents on lanes, 3 shared-union super-tiles")
+    p.add_argument("--tile-docs", type=int, default=0,
+                   help="kernel 1: 0 = 16 for fp32, 8 for fp16 codebooks; kernel 3: documents per super-tile")
     p.add_argument("--lane-neurons", type=int, default=0)
     p.add_argument("--group-tiles", type=int, default=0)
     p.add_argument("--mask-mode", type=int, default=0)
@@ -138,13 +140,14 @@ def main():
     # launch configuration: the library's defaults, except 16-document tiles for
     # an fp32 codebook (measured 5% faster on the 512^2 map; fp16 keeps 8)
     tile_docs = args.tile_docs or (8 if args.weights == "f16" or args.kernel == 2 else 16)
-    if args.kernel == 2:
+    if args.kernel in (2, 3):
         tile_docs = args.tile_docs
     knobs = dict(kernel=args.kernel, tile_docs=tile_docs, lane_neurons=args.lane_neurons,
                  group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons)
     kernel = args.kernel or 1
-    # documents that share one sweep of a union: a kernel-1 tile or a kernel-2 group
-    T = (tile_docs or 8) if kernel == 1 else 64 * (args.group_tiles or 16)
+    # documents that share one sweep of a union: a kernel-1 tile, a kernel-2
+    # group or a kernel-3 super-tile
+    T = {1: tile_docs or 8, 2: 64 * (args.group_tiles or 16), 3: tile_docs or 128}[kernel]
     cl_ws = torch.empty(max(som.som_cluster_workspace_bytes(B, F, nnz), 1), dtype=torch.uint8, device=dev)
     s_ws = torch.empty(max(som.som_bmu_search_planned_workspace_bytes(N, B, **knobs), 1),
                        dtype=torch.uint8, device=dev)
@@ -236,7 +239,7 @@ def main():
 
     # union sizes of this run's tiles/groups (the plan's per-unit counts)
     ntiles = (B + T - 1) // T
-    if kernel == 1:
+    if kernel in (1, 3):
         cnt = som.som_tile_plan(ip, ix, F, T, perm=perm)[1]
     else:
         cnt = som.som_group_plan(ip, ix, F, T, perm=perm)[1]
@@ -321,7 +324,8 @@ def main():
         },
         "roofline": {
             "kernel": ("k_search (union sweep writing the distance block) + k_argmin_rows" if args.unfused else
-                       ("k_search_docs" if kernel == 2 else "k_search") + " (fused union sweep + argmin) with key init and decode"),
+                       {1: "k_search", 2: "k_search_docs", 3: "k_search_st"}[kernel]
+                       + " (fused union sweep + argmin) with key init and decode"),
             "bound": "l2",
             "achieved": l2_bytes / search_s / 1e9,
             "peak": L2_PEAK_BPS / 1e9,

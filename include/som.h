@@ -64,17 +64,26 @@ typedef enum som_status {
  * kernel 2, documents on lanes: a workgroup holds a group of 64*G documents,
  *   one per lane, against a narrow slice of NB neurons; the group's feature
  *   union (the tile union with a tile of 64*G documents) streams through LDS
- *   and each lane adds the rows of its own document's features.
- * Either way the neuron axis is cut into slices whose minima are merged
- * (Section 4.2) and the argmin is fused (Section 3). */
+ *   and each lane adds the rows of its own document's features;
+ * kernel 3, shared-union super-tiles: a workgroup holds a super-tile of D
+ *   documents (tile_docs: 64, 128 or 256) against 256 neurons (fp32) or 512
+ *   (fp16); the super-tile's union (Section 4.1 with a tile of D documents)
+ *   is fetched once per workgroup with 128-bit loads into LDS, and each wave
+ *   (16 documents for fp32, 8 for fp16) adds the rows its documents hold.
+ *   Its plan is the tile plan with D-document tiles; a plan built with the
+ *   same tile_docs serves both storage types.
+ * Every kernel cuts the neuron axis into slices whose minima are merged
+ * (Section 4.2) and fuses the argmin (Section 3). */
 typedef struct som_bmu_opts {
-  int32_t kernel;        /* 0 = auto (kernel 1), 1 = neurons on lanes, 2 = documents on lanes */
-  int32_t tile_docs;     /* kernel 1: T = 0 (auto: 8), 1, 2, 4, 8, 16 or 32 */
+  int32_t kernel;        /* 0 = auto (kernel 1), 1 = neurons on lanes, 2 = documents on lanes,
+                            3 = shared-union super-tiles */
+  int32_t tile_docs;     /* kernel 1: T = 0 (auto: 8), 1, 2, 4, 8, 16 or 32;
+                            kernel 3: D = 0 (auto: 64), 64, 128 or 256 (256: fp32 only) */
   int32_t lane_neurons;  /* kernel 1: K = 0 (auto: 4), 4 or 8; T = 32 needs 4 */
   int32_t group_tiles;   /* kernel 1: tiles per workgroup, 0 (auto), 1, 2, 4 or 8;
                             kernel 2: waves per workgroup G, 0 (auto), 4, 8 or 16 */
   int32_t mask_mode;     /* kernel 1: 0 = auto, 1 = branch-free multiply by the membership
-                            bit, 2 = one scalar branch per document */
+                            bit, 2 = one scalar branch per document; kernel 3: 0 */
   int32_t slice_neurons; /* kernel 2: NB = 0 (auto), 32 or 64 */
   int32_t validate;      /* 1 = check the CSR batch on the device first (synchronises `stream`) */
   int32_t reserved;      /* must be 0 */
@@ -185,14 +194,16 @@ som_status som_bmu_search_top2_planned(const float* W, int64_t F, int64_t N, int
  * tile of T consecutive documents of the tiled order (perm as in
  * som_bmu_search; the last tile may be short) the sorted union of their
  * features and, per union entry, a T-bit membership mask (bit s set iff the
- * tile's s-th document contains the feature).
- *   tile_docs   T in {1, 2, 4, 8, 16, 32}
+ * tile's s-th document contains the feature).  This is also the plan of
+ * kernel 3 (tiles of its D documents).
+ *   tile_docs   T in {1, 2, 4, 8, 16, 32, 64, 128, 256}
  *   tile_offset int32 [ntiles+1] output, ntiles = ceil(B / T): tile t's union
  *               is stored at [tile_offset[t], tile_offset[t] + tile_count[t]);
  *               tile_offset[t] is the number of nonzeros of tiles < t
  *   tile_count  int32 [ntiles] output: |U_t|
  *   union_feat  int32 [nnz] output (entries past each tile's count are unused)
- *   union_mask  uint32 [nnz] output
+ *   union_mask  uint32 [nnz * MW] output, MW = ceil(T / 32) words per entry:
+ *               bit s of entry u is bit s % 32 of union_mask[u * MW + s / 32]
  * Needs no workspace. */
 som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                          int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,

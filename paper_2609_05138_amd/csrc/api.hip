@@ -83,10 +83,10 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
   som_bmu_opts o{};
   if (opts) o = *opts;
   const bool f16 = weights == som::kWeightsF16;
-  if (f16 && o.kernel == 2) return fail(SOM_ERR_INVALID_ARG, "an fp16 codebook is searched by kernel 1 only");
+  if (f16 && o.kernel == 2) return fail(SOM_ERR_INVALID_ARG, "an fp16 codebook is searched by kernels 1 and 3 only");
   if (o.reserved != 0) return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
   if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
-  if (o.kernel < 0 || o.kernel > 2) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1 or 2");
+  if (o.kernel < 0 || o.kernel > 3) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1, 2 or 3");
   const int kernel = o.kernel ? o.kernel : 1;
   p->kernel = kernel;
   if (kernel == 1) {
@@ -109,9 +109,26 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
     p->mask_mode = o.mask_mode == 2 ? 1 : (o.mask_mode == 1 ? 0 : (T <= 4 ? 0 : 1));
     p->D = T;
     p->nchunks = (N + 64 * K - 1) / (64 * K);
+  } else if (kernel == 3) {
+    // super-tile of D documents; waves of 16 (fp32) or 8 (fp16) documents
+    if (o.group_tiles || o.mask_mode || o.slice_neurons)
+      return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles, mask_mode and slice_neurons must be 0 for kernel 3");
+    const int D = o.tile_docs ? o.tile_docs : 64;
+    if (D != 64 && D != 128 && D != 256)
+      return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 64, 128 or 256 for kernel 3");
+    if (f16 && D == 256) return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs 256 is not available for an fp16 codebook");
+    const int K = f16 ? 8 : 4;
+    if (o.lane_neurons && o.lane_neurons != K)
+      return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0 (or 4 for fp32, 8 for fp16) for kernel 3");
+    p->T = f16 ? 8 : 16;
+    p->K = K;
+    p->group = D / p->T;
+    p->mask_mode = 1;
+    p->D = D;
+    p->nchunks = (N + 64 * K - 1) / (64 * K);
   } else {
     if (o.tile_docs || o.lane_neurons || o.mask_mode)
-      return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs, lane_neurons and mask_mode apply to kernel 1 only");
+      return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs, lane_neurons and mask_mode apply to kernels 1 and 3 only");
     const int G = o.group_tiles ? o.group_tiles : 16;
     if (G != 4 && G != 8 && G != 16)
       return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles must be 0, 4, 8 or 16 for kernel 2");
@@ -138,7 +155,7 @@ size_t take(size_t& o, size_t bytes) {
 
 // Plan layout (each region 256-byte aligned): offsets [nunits+1], counts
 // [nunits], union features [nnz], then kernel 1 masks or kernel 2 entry
-// positions [nnz].
+// positions [nnz]; kernel 3: features [nnz + 256], masks [nnz + 256][D / 32].
 struct PlanLayout {
   size_t offset, count, feat, extra, total;
 };
@@ -148,8 +165,11 @@ PlanLayout plan_layout(const Plan& p, int64_t nnz) {
   size_t o = 0;
   l.offset = take(o, sizeof(int32_t) * (p.nunits + 1));
   l.count = take(o, sizeof(int32_t) * p.nunits);
-  l.feat = take(o, sizeof(int32_t) * nnz);
-  l.extra = take(o, sizeof(int32_t) * nnz);
+  // kernel 3 reads whole stages, and feature ids a few stages ahead, past a
+  // union's end
+  const int64_t pad = p.kernel == 3 ? 256 : 0;
+  l.feat = take(o, sizeof(int32_t) * (nnz + pad));
+  l.extra = take(o, sizeof(int32_t) * (p.kernel == 3 ? (nnz + pad) * (p.D / 32) : nnz));
   l.total = o;
   return l;
 }
@@ -201,8 +221,8 @@ som_status run_validate(const int32_t* indptr, const int32_t* indices, int64_t B
 hipError_t build_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                       const int32_t* perm, const Plan& p, void* plan, const PlanLayout& l,
                       hipStream_t stream) {
-  if (p.kernel == 1)
-    return som::launch_tile_plan(indptr, indices, B, F, perm, p.T, at<int32_t>(plan, l.offset),
+  if (p.kernel == 1 || p.kernel == 3)
+    return som::launch_tile_plan(indptr, indices, B, F, perm, static_cast<int>(p.D), at<int32_t>(plan, l.offset),
                                  at<int32_t>(plan, l.count), at<int32_t>(plan, l.feat),
                                  at<uint32_t>(plan, l.extra), stream);
   return som::launch_group_plan(indptr, indices, B, F, perm, static_cast<int>(p.D),
@@ -234,7 +254,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
   a.nchunks = p.nchunks;
   a.tile_base = 0;
   a.tile_end = p.nunits;
-  if (p.kernel == 1) {
+  if (p.kernel == 1 || p.kernel == 3) {
     a.tile_offset = at<int32_t>(plan, l.offset);
     a.tile_count = at<int32_t>(plan, l.count);
     a.union_feat = at<int32_t>(plan, l.feat);
@@ -264,7 +284,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 9; }
+int32_t som_abi_version(void) { return 10; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -483,8 +503,8 @@ som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t 
   if (s != SOM_OK) return s;
   if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
   const int T = tile_docs;
-  if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
-    return fail(SOM_ERR_INVALID_ARG, "tile_docs must be 1, 2, 4, 8, 16 or 32");
+  if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32 && T != 64 && T != 128 && T != 256)
+    return fail(SOM_ERR_INVALID_ARG, "tile_docs must be 1, 2, 4, 8, 16, 32, 64, 128 or 256");
   if ((B + T - 1) / T >= kMaxTiles)
     return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: ceil(B/T) must be < 2^24");
   if (B == 0) return ok();

@@ -67,9 +67,10 @@ struct SearchArgs {
   const int32_t* indptr;
   const int32_t* perm;
   int64_t B;
-  int T;            // documents per tile
+  int T;            // documents per tile (kernel 3: per wave)
   int K;            // neurons per lane (4 or 8); a slice is 64 * K neurons
   int group;        // tiles (waves) per workgroup, all on the same slice
+                    // (kernel 3: waves per super-tile of group * T documents)
   int mask_mode;    // 0 = branch-free fma by the membership bit, 1 = scalar branches
   int64_t ntiles;
   int64_t nchunks;  // neuron slices = ceil(N / (64 * K))
@@ -84,7 +85,8 @@ struct SearchArgs {
   uint64_t* keys;   // [B] packed (distance, index) minima, tiled order
   uint64_t* keys2;  // [B] second-smallest keys, or nullptr when only the BMU is wanted
   // documents-on-lanes search (kernel 2)
-  int kernel;       // 1 = neurons on lanes (tile masks), 2 = documents on lanes (groups)
+  int kernel;       // 1 = neurons on lanes (tile masks), 2 = documents on lanes (groups),
+                    // 3 = shared-union super-tiles (tile plan with group * T / 32 mask words)
   int slice;        // kernel 2: neurons per slice (32 or 64)
   const int32_t* group_offset;
   const int32_t* group_count;
@@ -97,8 +99,9 @@ struct SearchArgs {
 };
 
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream);
-// Kernel 1 over an fp16 codebook (its own translation unit).
+// Kernels 1 and 3 over an fp16 codebook (their own translation unit).
 hipError_t launch_search_k1_f16(const SearchArgs& a, hipStream_t stream);
+hipError_t launch_search_st_f16(const SearchArgs& a, hipStream_t stream);
 // Unfused comparator: kernel 1 writes the distance block of block_docs
 // documents at a time into `score`, then a wave-per-row argmin reduces it.
 hipError_t launch_unfused(SearchArgs a, int64_t block_docs, hipStream_t stream);

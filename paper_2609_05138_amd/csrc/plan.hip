@@ -10,10 +10,11 @@
 //                     union of tile t is stored from there, and since
 //                     |U_t| <= nnz(t) it never overlaps tile t + 1
 //   tile_count[t]   = |U_t|
-//   union_feat[.]   = ascending feature ids, union_mask[.] (uint32) = masks
+//   union_feat[.]   = ascending feature ids, union_mask[. * MW + w] (uint32)
+//                     = word w of the entry's mask
 //
 // Construction: one workgroup per tile marks a bitmap of T-bit masks indexed
-// by feature (a window of up to 32768 features in LDS), then compacts the
+// by feature (a window of up to 32768 / MW features in LDS), then compacts the
 // nonzero entries in ascending order with a workgroup prefix sum.  Integer
 // work, bit-exact by construction.
 #include "common.h"
@@ -91,10 +92,10 @@ __device__ int32_t block_exclusive_scan(int32_t v, int32_t* tmp, int32_t* total)
 
 __global__ void __launch_bounds__(kPlanThreads)
 k_plan(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
-       const int32_t* __restrict__ perm, int64_t B, int64_t F, int T, int window,
+       const int32_t* __restrict__ perm, int64_t B, int64_t F, int T, int MW, int window,
        const int32_t* __restrict__ tile_offset, int32_t* __restrict__ tile_count,
        int32_t* __restrict__ union_feat, uint32_t* __restrict__ union_mask) {
-  extern __shared__ uint32_t bits[];  // [window]
+  extern __shared__ uint32_t bits[];  // [window][MW]
   __shared__ int32_t tmp[kPlanThreads];
   const int tid = threadIdx.x;
   const int64_t t = blockIdx.x;
@@ -102,7 +103,7 @@ k_plan(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
   int32_t written = 0;
   for (int64_t w0 = 0; w0 < F; w0 += window) {
     const int wlen = static_cast<int>(F - w0 < window ? F - w0 : window);
-    for (int i = tid; i < wlen; i += kPlanThreads) bits[i] = 0u;
+    for (int i = tid; i < wlen * MW; i += kPlanThreads) bits[i] = 0u;
     __syncthreads();
     for (int k = 0; k < T; ++k) {
       const int64_t p = t * T + k;
@@ -111,7 +112,7 @@ k_plan(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
       const int32_t a = indptr[d], b = indptr[d + 1];
       for (int32_t i = a + tid; i < b; i += kPlanThreads) {
         const int64_t f = indices[i];
-        if (f >= w0 && f < w0 + wlen) atomicOr(&bits[f - w0], 1u << k);
+        if (f >= w0 && f < w0 + wlen) atomicOr(&bits[(f - w0) * MW + (k >> 5)], 1u << (k & 31));
       }
     }
     __syncthreads();
@@ -120,15 +121,20 @@ k_plan(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int a = tid * per;
     const int b = a + per < wlen ? a + per : wlen;
     int32_t cnt = 0;
-    for (int i = a; i < b; ++i) cnt += bits[i] != 0u;
+    for (int i = a; i < b; ++i) {
+      uint32_t any = 0u;
+      for (int w = 0; w < MW; ++w) any |= bits[i * MW + w];
+      cnt += any != 0u;
+    }
     int32_t total;
     int32_t pos = block_exclusive_scan(cnt, tmp, &total);
     for (int i = a; i < b; ++i) {
-      const uint32_t m = bits[i];
-      if (m) {
+      uint32_t any = 0u;
+      for (int w = 0; w < MW; ++w) any |= bits[i * MW + w];
+      if (any) {
         const int64_t o = out0 + written + pos;
         union_feat[o] = static_cast<int32_t>(w0 + i);
-        union_mask[o] = m;
+        for (int w = 0; w < MW; ++w) union_mask[o * MW + w] = bits[i * MW + w];
         ++pos;
       }
     }
@@ -282,14 +288,15 @@ hipError_t launch_tile_plan(const int32_t* indptr, const int32_t* indices, int64
   hipLaunchKernelGGL(k_tile_nnz, dim3(static_cast<uint32_t>((ntiles + 255) / 256)), dim3(256), 0,
                      stream, indptr, perm, B, T, ntiles, tile_count);
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, tile_count, ntiles, tile_offset);
-  const int window = static_cast<int>(F < kPlanWindow ? F : kPlanWindow);
-  const size_t lds = sizeof(uint32_t) * static_cast<size_t>(window);
+  const int MW = (T + 31) / 32;
+  const int window = static_cast<int>(F < kPlanWindow / MW ? F : kPlanWindow / MW);
+  const size_t lds = sizeof(uint32_t) * static_cast<size_t>(window) * MW;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_plan),
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      static_cast<int>(lds));
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_plan, dim3(static_cast<uint32_t>(ntiles)), dim3(kPlanThreads), lds, stream,
-                     indptr, indices, perm, B, F, T, window, tile_offset, tile_count, union_feat,
+                     indptr, indices, perm, B, F, T, MW, window, tile_offset, tile_count, union_feat,
                      union_mask);
   return hipGetLastError();
 }

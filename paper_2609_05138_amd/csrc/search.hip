@@ -1,7 +1,7 @@
 // Fused BMU search, kernel 2 (documents on lanes), the key array
-// initialisation and decode, and the dispatch of both kernels (paper,
-// Section 3; kernel 1 is in search_k1.h).
-#include "search_k1.h"
+// initialisation and decode, and the dispatch of the three kernels (paper,
+// Section 3; kernel 1 is in search_k1.h, kernel 3 in search_st.h).
+#include "search_st.h"
 
 namespace som {
 namespace {
@@ -266,10 +266,22 @@ hipError_t launch_k1(const SearchArgs& a, hipStream_t stream) {
   }
 }
 
+hipError_t launch_k3(const SearchArgs& a, hipStream_t stream) {
+  if (a.weights == kWeightsF16) return launch_search_st_f16(a, stream);
+  if (a.T != 16 || a.K != 4) return hipErrorInvalidValue;
+  switch (a.group) {
+    case 4: return launch_st<float, 16, 4, 4>(a, stream);
+    case 8: return launch_st<float, 16, 4, 8>(a, stream);
+    case 16: return launch_st<float, 16, 4, 16>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(k_keys_init, dim3(static_cast<uint32_t>((a.B + 255) / 256)), dim3(256), 0, stream,
                      a.keys, a.keys2, a.B);
   if (a.kernel == 2) return launch_docs(a, stream);
+  if (a.kernel == 3) return launch_k3(a, stream);
   return launch_k1(a, stream);
 }
 

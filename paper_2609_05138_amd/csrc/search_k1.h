@@ -155,6 +155,9 @@ struct Storage<_Float16> {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float8 __attribute__((ext_vector_type(8)));
+// A native 128-bit vector (HIP's uint4 is a struct whose copies can go through
+// private memory when staged in arrays).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Widen one 128-bit load of the storage type to fp32 (exact for fp16).
 template <typename WT>
@@ -170,6 +173,93 @@ __device__ __forceinline__ void widen<_Float16>(const uint4& raw, float4* out) {
   const float8 f = __builtin_convertvector(h, float8);
   out[0] = make_float4(f[0], f[1], f[2], f[3]);
   out[1] = make_float4(f[4], f[5], f[6], f[7]);
+}
+template <typename WT>
+__device__ __forceinline__ void widen_v(const u32x4& raw, float4* out);
+template <>
+__device__ __forceinline__ void widen_v<float>(const u32x4& raw, float4* out) {
+  out[0] = make_float4(__uint_as_float(raw.x), __uint_as_float(raw.y), __uint_as_float(raw.z),
+                       __uint_as_float(raw.w));
+}
+template <>
+__device__ __forceinline__ void widen_v<_Float16>(const u32x4& raw, float4* out) {
+  const half8 h = __builtin_bit_cast(half8, raw);
+  const float8 f = __builtin_convertvector(h, float8);
+  out[0] = make_float4(f[0], f[1], f[2], f[3]);
+  out[1] = make_float4(f[4], f[5], f[6], f[7]);
+}
+
+// Fused epilogue (Section 3): the T documents at tiled positions p0 .. p0+T-1
+// against this wave's slice of 64*K neurons starting at n0.  Distances
+// (|S| + ||w_j||^2) - 2*dot are formed in registers, reduced per lane (ascending
+// j, strict < keeps the lowest index), then across the wave with shuffles, and
+// folded into the document's packed key with one 64-bit atomic minimum (or, for
+// the top-2 search, into the (best, second) pair; for the unfused comparator,
+// written to the distance block instead).
+template <typename WT, int T, int K>
+__device__ __forceinline__ void epilogue(const SearchArgs& a, const float (&acc)[T][K], int64_t p0, int64_t n0,
+                                         int lane) {
+  constexpr int E = Storage<WT>::kE;
+  constexpr int Q = K / E;
+  float nrm[K];
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int64_t j = n0 + 64 * E * q + E * lane + e;
+      nrm[E * q + e] = j < a.N ? a.norms[j] : 0.f;
+    }
+#pragma unroll
+  for (int s = 0; s < T; ++s) {
+    const int64_t p = p0 + s;
+    if (p >= a.B) break;
+    const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
+    const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
+    if (a.score) {  // unfused comparator: write the distances, no argmin here
+      float* row = a.score + (p - a.tile_base * T) * a.N;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int64_t j = n0 + 64 * E * q + E * lane + e;
+          if (j < a.N) row[j] = fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]);
+        }
+      continue;
+    }
+    if (a.keys2) {  // best and second best (wave-uniform branch)
+      uint64_t k1 = kNoKey, k2 = kNoKey;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int64_t j = n0 + 64 * E * q + E * lane + e;
+          if (j < a.N)
+            top2_insert(pack_key(fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]), static_cast<uint32_t>(j)),
+                        k1, k2);
+        }
+      wave_top2_u64(k1, k2);
+      if (lane == 0) top2_merge(a.keys + p, a.keys2 + p, k1, k2);
+      continue;
+    }
+    float best = 0.f;
+    uint32_t bj = 0xffffffffu;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int64_t j = n0 + 64 * E * q + E * lane + e;
+        if (j < a.N) {
+          const float dj = fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]);
+          if (bj == 0xffffffffu || dj < best) {  // ascending j: strict < keeps the lowest
+            best = dj;
+            bj = static_cast<uint32_t>(j);
+          }
+        }
+      }
+    uint64_t key = bj == 0xffffffffu ? kNoKey : pack_key(best, bj);
+    key = wave_min_u64(key);
+    if (lane == 0) atomicMin(reinterpret_cast<unsigned long long*>(a.keys + p), static_cast<unsigned long long>(key));
+  }
 }
 
 template <typename WT, int T, int K, int G, int U, int MODE>
@@ -266,65 +356,7 @@ k_search(SearchArgs a) {
     }
   }
 
-  float nrm[K];
-#pragma unroll
-  for (int q = 0; q < Q; ++q)
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int64_t j = n0 + 64 * E * q + E * lane + e;
-      nrm[E * q + e] = j < a.N ? a.norms[j] : 0.f;
-    }
-#pragma unroll
-  for (int s = 0; s < T; ++s) {
-    const int64_t p = t * T + s;
-    if (p >= a.B) break;
-    const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
-    const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
-    if (a.score) {  // unfused comparator: write the distances, no argmin here
-      float* row = a.score + (p - a.tile_base * T) * a.N;
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const int64_t j = n0 + 64 * E * q + E * lane + e;
-          if (j < a.N) row[j] = fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]);
-        }
-      continue;
-    }
-    if (a.keys2) {  // best and second best (wave-uniform branch)
-      uint64_t k1 = kNoKey, k2 = kNoKey;
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const int64_t j = n0 + 64 * E * q + E * lane + e;
-          if (j < a.N)
-            top2_insert(pack_key(fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]), static_cast<uint32_t>(j)),
-                        k1, k2);
-        }
-      wave_top2_u64(k1, k2);
-      if (lane == 0) top2_merge(a.keys + p, a.keys2 + p, k1, k2);
-      continue;
-    }
-    float best = 0.f;
-    uint32_t bj = 0xffffffffu;
-#pragma unroll
-    for (int q = 0; q < Q; ++q)
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int64_t j = n0 + 64 * E * q + E * lane + e;
-        if (j < a.N) {
-          const float dj = fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]);
-          if (bj == 0xffffffffu || dj < best) {  // ascending j: strict < keeps the lowest
-            best = dj;
-            bj = static_cast<uint32_t>(j);
-          }
-        }
-      }
-    uint64_t key = bj == 0xffffffffu ? kNoKey : pack_key(best, bj);
-    key = wave_min_u64(key);
-    if (lane == 0) atomicMin(reinterpret_cast<unsigned long long*>(a.keys + p), static_cast<unsigned long long>(key));
-  }
+  epilogue<WT, T, K>(a, acc, t * T, n0, lane);
 }
 
 template <typename WT, int T, int K, int G>

@@ -1,0 +1,222 @@
+// Kernel 3 of the fused BMU search: a shared-union super-tile.
+//
+// The union sweep of Section 4.1 reads each union row slice once per tile,
+// so the rows that many tiles hold (the head of the feature law) are
+// requested from L2 once per tile, and the tile size that keeps a wave's
+// accumulators in VGPRs (T documents x K neurons per lane) caps the sharing.
+// Here a workgroup of S waves takes a super-tile of D = S*T consecutive
+// documents of the tiled order and one neuron slice of 64*K neurons: the
+// super-tile's union (its own plan, D-bit membership masks) is swept once,
+// each row slice fetched once per workgroup (one 1 KB row per wave
+// instruction, 16 bytes per lane) straight into LDS, and every wave adds
+// from LDS the rows that its own T documents hold.  Wave w owns documents
+// w*T .. w*T+T-1 of the super-tile and their T x K accumulators, exactly as a
+// kernel-1 wave owns a tile; its T-bit slice of each entry's mask drives the
+// same wave-uniform dispatch, and its documents' dot products are summed in
+// ascending feature order, so the results are bit-identical to kernel 1's.
+//
+// Pipeline: the union is cut into stages of P entries held in a ring of
+// NSLOT LDS slots.  Each wave moves its P/S rows of a stage, and its own
+// T-bit mask word of each of the stage's entries, with direct global-to-LDS
+// loads (no registers), NSLOT-1 stages ahead of the adds.  Before stage s is
+// added, each wave waits until its own loads of stage s have landed (a
+// vector-memory count: the loads of the later stages may stay in flight),
+// then one barrier makes every wave's part visible and closes stage s-1,
+// whose slot the loads of stage s+NSLOT-1 then reuse.  The feature ids of
+// those loads arrive with stage s itself (spare lanes of its mask load).  Entries past the
+// union's end load row 0 and get empty masks.  A wave skips the entries of a
+// stage its documents do not hold: a ballot over the stage's masks (lane r
+// holds entry r's word) gives the needed entries, visited in ascending order
+// with the next row's LDS read issued before the current row's adds.
+//
+// Included by the translation units that instantiate it; internal linkage.
+#pragma once
+
+#include "search_k1.h"
+
+namespace som {
+namespace {
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// Byte offset of a __shared__ object in the workgroup's LDS.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)(const_cast<void*>(p))));
+}
+
+// Direct global-to-LDS loads: lane i's 16 (or 4) bytes at `src` land at LDS
+// byte m0 + 16*i (or 4*i); `m0` must be wave-uniform.  The loads count in the
+// vector-memory counter like any load and write LDS when they return.  They
+// are issued by inline assembly so that the compiler's own wait insertion
+// (which cannot tell ring slots apart) does not drain them at every LDS
+// read; the kernel waits for them itself (vm_wait) before its barriers.
+__device__ __forceinline__ void dma_b128(const void* src, uint32_t m0) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+}
+__device__ __forceinline__ void dma_b32(const void* src, uint32_t m0) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait until at most `n` of this wave's stages are still in flight (OPS
+// loads per stage); n is wave-uniform and at most NSLOT - 2.
+template <int OPS, int NSLOT>
+__device__ __forceinline__ void wait_stages(int n) {
+  static_assert(NSLOT >= 2 && NSLOT <= 6 && (NSLOT - 2) * OPS < 64, "ring depth");
+  if (NSLOT > 5 && n >= 4) return vm_wait<(NSLOT > 5 ? 4 : 0) * OPS>();
+  if (NSLOT > 4 && n >= 3) return vm_wait<(NSLOT > 4 ? 3 : 0) * OPS>();
+  if (NSLOT > 3 && n >= 2) return vm_wait<(NSLOT > 3 ? 2 : 0) * OPS>();
+  if (NSLOT > 2 && n >= 1) return vm_wait<(NSLOT > 2 ? 1 : 0) * OPS>();
+  vm_wait<0>();
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <typename WT, int T, int K, int S, int P, int NSLOT>
+__global__ void __launch_bounds__(S * 64)
+k_search_st(SearchArgs a) {
+  constexpr int E = Storage<WT>::kE;  // elements per 128-bit load
+  static_assert(K == E, "one 128-bit load per lane per row: a row slice is 1 KB");
+  static_assert(T <= 16 && S * T <= 256, "wave masks fit 16 bits, super-tile masks 8 words");
+  static_assert(P <= 32 && P % S == 0 && (P & (P - 1)) == 0, "a stage's masks and ids fit one per lane");
+  static_assert(NSLOT * P <= 192, "ids read ahead stay inside the plan's padding");
+  constexpr int64_t WN = 64 * K;      // neurons per slice
+  constexpr int D = S * T;            // documents per super-tile
+  constexpr int MW = (D + 31) / 32;   // mask words per union entry
+  constexpr int RPW = P / S;          // rows each wave loads per stage
+  constexpr int OPS = RPW + 1;        // loads per wave per stage (rows + mask words)
+  __shared__ u32x4 ring[NSLOT][P][64];      // row slices
+  __shared__ uint32_t mring[NSLOT][S][64];  // per wave: its mask word of each entry
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // XCD-contiguous super-tile ranges (see k_search)
+  const uint32_t per_xcd = gridDim.x / kXcds;
+  const int64_t st = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  const int64_t c = blockIdx.y;
+  if (st >= a.ntiles) return;  // whole workgroup: no barrier is skipped by part of it
+
+  const int64_t n0 = c * WN;
+  float acc[T][K];
+#pragma unroll
+  for (int s = 0; s < T; ++s)
+#pragma unroll
+    for (int k = 0; k < K; ++k) acc[s][k] = 0.f;
+
+  // lanes past the row end re-read the row's last 128-bit group (in bounds)
+  const int64_t o = E * lane;
+  const uint32_t offb = static_cast<uint32_t>(sizeof(WT) * (n0 + o < a.ldw ? o : a.ldw - E - n0));
+  const char* __restrict__ Wn = reinterpret_cast<const char*>(static_cast<const WT*>(a.W) + n0) + offb;
+  const int64_t ldw_b = a.ldw * static_cast<int64_t>(sizeof(WT));
+  const int32_t u0 = a.tile_offset[st];
+  const int32_t cnt = a.tile_count[st];
+  // The plan pads its feature and mask arrays by 256 entries, so every read
+  // of a whole stage (or of the ids NSLOT-1 stages ahead) stays inside it.
+  // (The prologue reads ids through the constant address space: scalar loads,
+  // which the vector-memory waits of the ring never drain.)
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
+  const const_i32 feat = (const_i32)(a.union_feat + u0);
+  const int mword = (wave * T) >> 5;
+  const int mshift = (wave * T) & 31;
+  constexpr uint32_t kWaveBits = (1u << T) - 1u;
+  // Each stage's dword load carries, per lane: lanes r < P the wave's mask
+  // word of entry r of the stage; lanes P + r the feature id of entry r of the
+  // stage NSLOT-1 later (so the row loads issued after a stage's barrier need
+  // no scalar load); other lanes repeat lane r & (P-1)'s word.
+  const bool id_lane = lane >= P && lane < 2 * P;
+  const uint32_t* __restrict__ dsrc =
+      id_lane ? reinterpret_cast<const uint32_t*>(a.union_feat + u0 + (NSLOT - 1) * P + (lane - P))
+              : a.union_mask + (static_cast<int64_t>(u0) + (lane & (P - 1))) * MW + mword;
+  const int64_t dstride = id_lane ? P : static_cast<int64_t>(P) * MW;  // words per stage
+  const int32_t nstages = (cnt + P - 1) / P;
+  const uint32_t ring0 = lds_offset(&ring[0][0][0]) + static_cast<uint32_t>(wave * RPW * 1024);
+  const uint32_t mring0 = lds_offset(&mring[0][0][0]) + static_cast<uint32_t>(wave * 256);
+
+  if (nstages > 0) {
+    // stage q into slot q % NSLOT: this wave's rows (feature ids fid[i]), then
+    // its dword load (mask words, ids of stage q + NSLOT - 1)
+#define SOM_ST_ISSUE(q, fid)                                                                  \
+  {                                                                                           \
+    const int32_t q_ = (q);                                                                   \
+    const uint32_t slot_ = static_cast<uint32_t>(q_ % NSLOT);                                 \
+    _Pragma("unroll") for (int i = 0; i < RPW; ++i) {                                         \
+      const int32_t e = q_ * P + wave * RPW + i;                                              \
+      const int64_t f = e < cnt ? (fid)[i] : 0;                                               \
+      dma_b128(Wn + f * ldw_b, ring0 + slot_ * (P * 1024) + static_cast<uint32_t>(i * 1024)); \
+    }                                                                                         \
+    dma_b32(dsrc + q_ * dstride, mring0 + slot_ * (S * 256));                                 \
+  }
+#pragma unroll
+    for (int q = 0; q < NSLOT - 1; ++q) {
+      if (q < nstages) {
+        int32_t fid[RPW];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) fid[i] = feat[q * P + wave * RPW + i];
+        SOM_ST_ISSUE(q, fid)
+      }
+    }
+    for (int32_t s = 0; s < nstages; ++s) {
+      // this wave's stages issued after s: min(nstages - 1, s + NSLOT - 2) - s
+      const int32_t later = (nstages - 1 < s + NSLOT - 2 ? nstages - 1 : s + NSLOT - 2) - s;
+      wait_stages<OPS, NSLOT>(later);
+      lds_barrier();  // stage s visible to all waves; every wave is done with stage s-1
+      const int slot = s % NSLOT;
+      const uint32_t w = mring[slot][wave][lane];
+      if (s + NSLOT - 1 < nstages) {
+        int32_t fid[RPW];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) fid[i] = __builtin_amdgcn_readlane(static_cast<int>(w), P + wave * RPW + i);
+        SOM_ST_ISSUE(s + NSLOT - 1, fid)
+      }
+      const uint32_t m_cur = (lane < P && s * P + lane < cnt) ? (w >> mshift) & kWaveBits : 0u;
+      // this wave's needed entries of stage s, visited in ascending order
+      uint64_t need = __ballot(m_cur != 0u);
+      if (need) {
+        int r = __builtin_ctzll(need);
+        need &= need - 1;
+        u32x4 cur = ring[slot][r][lane];
+        uint32_t mc = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(m_cur), r));
+        while (need) {
+          const int r2 = __builtin_ctzll(need);
+          need &= need - 1;
+          const u32x4 nxt = ring[slot][r2][lane];
+          const uint32_t mn = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(m_cur), r2));
+          float4 wf[K / 4];
+          widen_v<WT>(cur, wf);
+          add_row<T, K, kMaskBranch>(acc, wf, mc);
+          cur = nxt;
+          mc = mn;
+        }
+        float4 wf[K / 4];
+        widen_v<WT>(cur, wf);
+        add_row<T, K, kMaskBranch>(acc, wf, mc);
+      }
+    }
+#undef SOM_ST_ISSUE
+  }
+
+  epilogue<WT, T, K>(a, acc, st * D + wave * T, n0, lane);
+}
+
+template <typename WT, int T, int K, int S>
+hipError_t launch_st(const SearchArgs& a, hipStream_t stream) {
+  // 16-entry stages in a ring of two: 32 KB of rows per workgroup, so up to
+  // five workgroups share a CU.  Measured on the 512^2 map (fp32, 262,144
+  // documents): the number of workgroups per CU decides the speed (each
+  // stage ends in a barrier that waits for the wave with the most rows);
+  // 32-entry stages and deeper rings (1 to 2 workgroups per CU) were slower.
+  constexpr int P = 16;
+  constexpr int NSLOT = 2;
+  const dim3 grid(static_cast<uint32_t>((a.ntiles + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));
+  hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT>), grid, dim3(S * 64), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace som

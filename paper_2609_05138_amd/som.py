@@ -373,7 +373,10 @@ def som_bmu_search_top2_planned(W: torch.Tensor, norms: torch.Tensor, indptr: to
 
 def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs: int = 8,
                   perm: Optional[torch.Tensor] = None, stream=None):
-    """Kernel-1 tile plan as explicit arrays: (tile_offset, tile_count, union_feat, union_mask)."""
+    """Tile plan as explicit arrays: (tile_offset, tile_count, union_feat, union_mask).
+
+    union_mask is int32 [nnz] for tile_docs <= 32, else [nnz, tile_docs // 32]
+    (bit s of the entry's mask in word s // 32)."""
     lib = load()
     _dev(indptr, torch.int32, "indptr")
     _dev(indices, torch.int32, "indices")
@@ -387,7 +390,8 @@ def som_tile_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, tile_docs
     tile_offset = torch.empty(ntiles + 1, dtype=torch.int32, device=dev)
     tile_count = torch.empty(max(ntiles, 1), dtype=torch.int32, device=dev)
     union_feat = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
-    union_mask = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    mw = (T + 31) // 32 if T > 0 else 1
+    union_mask = torch.empty((max(nnz, 1), mw) if mw > 1 else max(nnz, 1), dtype=torch.int32, device=dev)
     _check(lib.som_tile_plan(_ptr(indptr), _ptr(indices), B, F, nnz, _ptr(perm), T, _ptr(tile_offset),
                              _ptr(tile_count), _ptr(union_feat), _ptr(union_mask), _stream(stream)))
     return tile_offset, tile_count[:ntiles], union_feat, union_mask

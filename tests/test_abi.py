@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 9
+    assert som.som_abi_version() == 10
 
 
 def test_codebook_ldw_is_host_only(lib):
@@ -57,7 +57,7 @@ def test_codebook_ldw_is_host_only(lib):
 
 
 def test_workspace_sizes_are_host_only(lib):
-    for kernel in (0, 1, 2):
+    for kernel in (0, 1, 2, 3):
         o = som.som_bmu_opts(kernel)
         a = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(o))
         assert a > 0 and a % 256 == 0
@@ -69,9 +69,15 @@ def test_workspace_sizes_are_host_only(lib):
         v.validate = 1
         b = lib.som_bmu_workspace_bytes(20000, 262144, 1 << 20, 84_000_000, ctypes.byref(v))
         assert b > a                   # validation needs a scratch array
+    # kernel 3 (64-document super-tiles by default): two mask words per entry,
+    # plus a padding of 256 entries after the features and the masks
+    o = som.som_bmu_opts(3)
+    assert lib.som_plan_bytes(1 << 20, 84_000_000, ctypes.byref(o)) >= (4 + 8) * (84_000_000 + 256)
+    o = som.som_bmu_opts(3, 256)
+    assert lib.som_plan_bytes(1 << 20, 84_000_000, ctypes.byref(o)) >= (4 + 32) * (84_000_000 + 256)
     assert lib.som_bmu_workspace_bytes(0, 10, 10, 10, None) == 0
     assert lib.som_bmu_workspace_bytes(10, 10, -1, 10, None) == 0
-    bad = som.som_bmu_opts(3)
+    bad = som.som_bmu_opts(4)
     assert lib.som_bmu_workspace_bytes(10, 10, 10, 10, ctypes.byref(bad)) == 0
 
 
@@ -123,7 +129,8 @@ def test_search_rejects_bad_arguments(lib):
     res = som.som_bmu_opts()
     res.reserved = 1
     O = som.som_bmu_opts
-    for bad in (O(3), O(1, 5), O(1, 0, 3), res, O(1, 0, 0, 16), O(1, 0, 0, 0, 3), O(1, 32, 8),
+    for bad in (O(4), O(-1), O(3, 32), O(3, 16), O(3, 0, 8), O(3, 0, 0, 2), O(3, 0, 0, 0, 1), O(3, 0, 0, 0, 0, 32),
+                O(1, 5), O(1, 0, 3), res, O(1, 0, 0, 16), O(1, 0, 0, 0, 3), O(1, 32, 8),
                 O(0, 0, 0, 0, 0, 0, 2), O(1, 0, 0, -1), O(2, 8), O(2, 0, 4), O(2, 0, 0, 1),
                 O(2, 0, 0, 0, 1), O(2, 0, 0, 0, 0, 48), O(1, 0, 0, 0, 0, 32)):
         st, msg = call(opts=ctypes.byref(bad))
@@ -176,7 +183,7 @@ def test_f16_rejects_bad_arguments(lib):
 
     st, msg = call(ldw=12)                    # fine for fp32, not for fp16 (8 halves per load)
     assert st == som.SOM_ERR_INVALID_ARG and "multiple of 8" in msg
-    for bad in (O(2), O(1, 0, 4), O(1, 32), O(1, 32, 4)):
+    for bad in (O(2), O(1, 0, 4), O(1, 32), O(1, 32, 4), O(3, 256), O(3, 0, 4)):
         st, msg = call(opts=bad)
         assert st == som.SOM_ERR_INVALID_ARG, msg
     st, msg = _status(lib, "som_codebook_norms_f16", fake, 8, 12, 12, fake, null)
@@ -220,7 +227,7 @@ def test_unfused_rejects_bad_arguments(lib):
         return _status(lib, "som_bmu_search_unfused", fake, 8, 8, 8, fake, fake, fake, 4, 10, null, fake, fake,
                        ctypes.byref(o), block, fake, ws_bytes, null)
 
-    for bad in (dict(opts=O(2)), dict(block=0), dict(block=12), dict(block=-8)):
+    for bad in (dict(opts=O(2)), dict(opts=O(3)), dict(block=0), dict(block=12), dict(block=-8)):
         st, msg = call(**bad)
         assert st == som.SOM_ERR_INVALID_ARG, (bad, msg)
     assert call(ws_bytes=64)[0] == som.SOM_ERR_WORKSPACE

@@ -5,6 +5,8 @@ codebooks of 5.2 and 21 GB) the oracle cannot score a whole batch, so each
 test runs the device search on a full batch in the launch configuration the
 benchmark uses (kernel 1, 16-document tiles for fp32 and 8 for fp16, codebook
 rows at the recommended stride) and checks:
+  * that the shared-union super-tile kernel (kernel 3) returns bit-identical
+    results on the whole batch,
   * a seeded sample of documents (always including the first and the last)
     against the fp64 oracle under the acceptance rule, and
   * every document's reported distance against the fp64 distance of the
@@ -47,6 +49,11 @@ def _run(cfg_key, batch, cluster, sample, seed, top2=False, f16=False):
     norms = som.som_codebook_norms(Wd, N=cfg.N)
     perm = som.som_cluster_order(ip, ix, cfg.F) if cluster else None
     bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm, tile_docs=16)
+    # the shared-union super-tile kernel sums every dot product in the same
+    # order: bit-identical results on the whole batch
+    b3, d3 = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm, kernel=3)
+    assert torch.equal(b3, bmu) and torch.equal(d3, dist), "kernel 3 differs from kernel 1"
+    del b3, d3
     second = None
     if top2:   # the top-2 search on the same data: same first place, plus the second
         second = som.som_bmu_search_top2(Wd, norms, ip, ix, N=cfg.N, perm=perm, tile_docs=16)
@@ -57,7 +64,9 @@ def _run(cfg_key, batch, cluster, sample, seed, top2=False, f16=False):
         W16d = Wd.half()
         n16 = som.som_codebook_norms(W16d, N=cfg.N)
         half = [x.cpu().numpy() for x in som.som_bmu_search(W16d, n16, ip, ix, N=cfg.N, perm=perm, tile_docs=8)]
-        del W16d, n16
+        h3 = [x.cpu().numpy() for x in som.som_bmu_search(W16d, n16, ip, ix, N=cfg.N, perm=perm, kernel=3)]
+        assert np.array_equal(h3[0], half[0]) and np.array_equal(h3[1], half[1]), "fp16 kernel 3 differs"
+        del W16d, n16, h3
     torch.cuda.synchronize()
     bmu, dist = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
     if perm is not None:

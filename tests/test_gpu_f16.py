@@ -30,7 +30,8 @@ else:  # collected on CPU-only machines, never run there
 DEV = "cuda:0"
 REL = 1e-5
 KNOBS16 = [dict(), dict(tile_docs=1), dict(tile_docs=4), dict(tile_docs=16), dict(group_tiles=4),
-           dict(mask_mode=1), dict(kernel=1, lane_neurons=8, group_tiles=2)]
+           dict(mask_mode=1), dict(kernel=1, lane_neurons=8, group_tiles=2),
+           dict(kernel=3), dict(kernel=3, tile_docs=128)]
 
 
 def _csr(docs):
@@ -182,10 +183,16 @@ def test_f16_planned_search_shares_the_fp32_plan():
     n32 = som.som_codebook_norms(W32d, N=2048)
     n16 = som.som_codebook_norms(W16d, N=2048)
     assert torch.equal(n32, n16)
-    plan = som.som_plan(ip, ix, 20000)
-    a = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W32d, n32, ip, plan, N=2048)]
-    b = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W16d, n16, ip, plan, N=2048)]
-    c = [t.cpu().numpy() for t in som.som_bmu_search_planned(W16d, n16, ip, plan, N=2048)]
-    for x, y in zip(a, b):
-        assert np.array_equal(x, y)
-    assert np.array_equal(c[0], a[0]) and np.array_equal(c[1], a[1])
+    ref = None
+    for knobs in (dict(), dict(kernel=3), dict(kernel=3, tile_docs=128)):
+        # kernel 3: 16-document waves for fp32, 8 for fp16, the same super-tile plan
+        plan = som.som_plan(ip, ix, 20000, **knobs)
+        a = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W32d, n32, ip, plan, N=2048)]
+        b = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W16d, n16, ip, plan, N=2048)]
+        c = [t.cpu().numpy() for t in som.som_bmu_search_planned(W16d, n16, ip, plan, N=2048)]
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y), knobs
+        assert np.array_equal(c[0], a[0]) and np.array_equal(c[1], a[1]), knobs
+        ref = a if ref is None else ref
+        for x, y in zip(a, ref):
+            assert np.array_equal(x, y), knobs

@@ -72,6 +72,7 @@ def _random_docs(rng, B, F, mean, empty_every=0, big_every=0, big=0):
 
 
 TILES = [1, 2, 4, 8, 16, 32]
+SUPER = [64, 128, 256]          # kernel 3: documents per super-tile
 
 
 # ----------------------------------------------------------------------------
@@ -107,7 +108,8 @@ def test_norms_dyadic_bit_exact():
 # ----------------------------------------------------------------------------
 
 @pytest.mark.parametrize("knobs", [dict(kernel=1, tile_docs=T) for T in TILES]
-                         + [dict(kernel=2, group_tiles=G, slice_neurons=NB) for G in (4, 16) for NB in (32, 64)])
+                         + [dict(kernel=2, group_tiles=G, slice_neurons=NB) for G in (4, 16) for NB in (32, 64)]
+                         + [dict(kernel=3, tile_docs=D) for D in SUPER])
 def test_hand_examples_bit_exact(knobs):
     ex_all = json.load(open(os.path.join(GOLDEN, "hand_examples.json")))["examples"]
     for ex in ex_all:
@@ -139,7 +141,8 @@ def test_dyadic_codebook_bit_exact_with_ties(N):
     indptr, indices = _csr(docs)
     exact = oracle.bmu_search_exact(K, 2, indptr, indices)
     for knobs in (dict(kernel=1, tile_docs=1), dict(kernel=1, tile_docs=8), dict(kernel=1, tile_docs=32),
-                  dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64)):
+                  dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64),
+                  dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256)):
         bmu, dist, _ = _search(W, indptr, indices, **knobs)
         assert bmu.tolist() == [e[2][0] for e in exact]
         assert [Fraction(float(x)) for x in dist] == [Fraction(e[1], 16) for e in exact]
@@ -149,7 +152,14 @@ def test_dyadic_codebook_bit_exact_with_ties(N):
 # tile plan and clustering: integer work, bit-exact
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("T", TILES)
+def _mask_ints(um, T):
+    """Plan masks as Python ints (one uint32 word per entry up to 32
+    documents per tile, T / 32 words per entry beyond)."""
+    w = um.view(np.uint32).reshape(len(um), -1) if T > 32 else um.view(np.uint32).reshape(-1, 1)
+    return [sum(int(x) << (32 * k) for k, x in enumerate(row)) for row in w]
+
+
+@pytest.mark.parametrize("T", TILES + SUPER)
 def test_tile_plan_bit_exact(T):
     from synth import documents
     indptr, indices = documents(1, 0, n_docs=1001)      # ragged last tile
@@ -166,19 +176,20 @@ def test_tile_plan_bit_exact(T):
         for t, (feats, masks) in enumerate(tiles):
             assert cnt[t] == len(feats)
             assert uf[off[t]:off[t] + cnt[t]].tolist() == feats.tolist()
-            assert um[off[t]:off[t] + cnt[t]].view(np.uint32).tolist() == masks.astype(np.uint32).tolist()
+            assert _mask_ints(um[off[t]:off[t] + cnt[t]], T) == [int(m) for m in masks]
 
 
-def test_tile_plan_large_feature_ids_use_several_windows():
+@pytest.mark.parametrize("T", [4, 256])
+def test_tile_plan_large_feature_ids_use_several_windows(T):
     rng = np.random.default_rng(3)
-    F = 70_000                                         # > one 32768-feature window
-    docs = _random_docs(rng, 130, F, mean=30, empty_every=9)
+    F = 70_000                                         # > one 32768-feature window (4096 at T = 256)
+    docs = _random_docs(rng, 530, F, mean=30, empty_every=9)
     indptr, indices = _csr(docs)
-    pl = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), F, 4)
+    pl = som.som_tile_plan(_dev_i32(indptr), _dev_i32(indices), F, T)
     off, cnt, uf, um = (x.cpu().numpy() for x in pl)
-    for t, (feats, masks) in enumerate(oracle.tile_union(indptr, indices, 4)):
+    for t, (feats, masks) in enumerate(oracle.tile_union(indptr, indices, T)):
         assert uf[off[t]:off[t] + cnt[t]].tolist() == feats.tolist()
-        assert um[off[t]:off[t] + cnt[t]].view(np.uint32).tolist() == masks.astype(np.uint32).tolist()
+        assert _mask_ints(um[off[t]:off[t] + cnt[t]], T) == [int(m) for m in masks]
 
 
 @pytest.mark.parametrize("D", [1, 7, 256, 1024])
@@ -240,7 +251,7 @@ def test_config1_every_document():
     W = codebook(1)
     indptr, indices = documents(1, 0)
     for knobs in (dict(kernel=1, tile_docs=1), dict(kernel=1, tile_docs=8), dict(kernel=2),
-                  dict(kernel=2, group_tiles=4, slice_neurons=64)):
+                  dict(kernel=2, group_tiles=4, slice_neurons=64), dict(kernel=3), dict(kernel=3, tile_docs=256)):
         bmu, dist, _ = _search(W, indptr, indices, **knobs)
         W64 = W.astype(np.float64)
         _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, bmu, dist, range(len(indptr) - 1))
@@ -278,15 +289,16 @@ def test_results_identical_across_tile_chunk_and_order():
     for T in TILES:
         for K, G, mode in ((0, 0, 0), (4, 1, 1), (8 if T < 32 else 4, 8, 2), (4, 2, 2)):
             variants.append(dict(kernel=1, tile_docs=T, lane_neurons=K, group_tiles=G, mask_mode=mode))
+    variants += [dict(kernel=3, tile_docs=D) for D in SUPER]
     for i, v in enumerate(variants):
-        for perm in perms if i % 5 == 0 else perms[:2]:
+        for perm in perms if (i % 5 == 0 or v["kernel"] == 3) else perms[:2]:
             out = _search(W, indptr, indices, perm=perm, **v)
             if ref is None:
                 ref = out
             assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), v
     # the row stride is a layout choice only
     for ldw in (som.som_codebook_ldw(4100), 4104, 4100 + 1024):
-        for v in (dict(), dict(kernel=1, lane_neurons=8), dict(kernel=2)):
+        for v in (dict(), dict(kernel=1, lane_neurons=8), dict(kernel=2), dict(kernel=3)):
             out = _search(W, indptr, indices, ldw=ldw, **v)
             assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (ldw, v)
 

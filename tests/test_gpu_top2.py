@@ -31,7 +31,8 @@ REL = 1e-5
 
 KNOBS = [dict(kernel=1, tile_docs=T) for T in (1, 4, 8, 16, 32)] + [
     dict(kernel=1, lane_neurons=8), dict(kernel=1, group_tiles=4, mask_mode=1),
-    dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64)]
+    dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64),
+    dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256)]
 
 
 def _csr(docs):
@@ -122,7 +123,7 @@ def test_top2_single_neuron_has_no_second():
     rng = np.random.default_rng(3)
     W = rng.random((30, 1)).astype(np.float32)
     indptr, indices = _csr(_random_docs(rng, 70, 30, mean=5) + [[]])
-    for knobs in (dict(kernel=1), dict(kernel=2)):
+    for knobs in (dict(kernel=1), dict(kernel=2), dict(kernel=3)):
         bmu, dist, bmu2, dist2 = _top2(W, indptr, indices, **knobs)
         assert np.all(bmu == 0) and np.all(bmu2 == -1) and np.all(np.isinf(dist2)) and np.all(dist2 > 0)
 
@@ -165,7 +166,7 @@ def test_top2_config1_every_document():
     indptr, indices = documents(1, 0)
     W64 = W.astype(np.float64)
     norms64 = oracle.codebook_norms(W64)
-    for knobs in (dict(), dict(kernel=2)):
+    for knobs in (dict(), dict(kernel=2), dict(kernel=3)):
         bmu, dist, bmu2, dist2 = _top2(W, indptr, indices, **knobs)
         bad = []
         for d in range(len(indptr) - 1):
