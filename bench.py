@@ -72,6 +72,7 @@ def parse():
                    help="codebook storage (sums are fp32 either way)")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget (0 = skip)")
     p.add_argument("--check-docs", type=int, default=64, help="documents checked against the oracle")
+    p.add_argument("--no-probe", action="store_true", help="skip the in-run read-bandwidth probes")
     p.add_argument("--quiet", action="store_true")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run a device-to-device copy of MIB MiB (for scaling traffic counters)")
@@ -237,6 +238,29 @@ def main():
         log(args, f"update: accumulate {acc_ms:.3f} ms, finish {fin_ms:.3f} ms (sigma {args.sigma})")
         del acc, cnt, uws
 
+    # in-run roofs: read rates of an L2-resident buffer (16 or 32 MiB: 2 or 4
+    # MiB per XCD, the faster of the two), a memory-side-cache-resident one
+    # (192 MiB) and of the whole codebook from HBM (one pass), all with the
+    # library's probe kernel
+    probes = None
+    if not args.no_probe:
+        sink = torch.empty(1, dtype=torch.int32, device=dev)
+        wbytes_all = Wd.numel() * Wd.element_size()
+
+        def rate(nbytes, passes):
+            som.som_probe_read(Wd, nbytes, 1, sink)           # first touch (fills the caches)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            som.som_probe_read(Wd, nbytes, passes, sink)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return nbytes * passes / (e0.elapsed_time(e1) * 1e-3)
+
+        probes = {"l2_GBps": max(rate(16 << 20, 200), rate(32 << 20, 100)) / 1e9,
+                  "mall_GBps": rate(192 << 20, 20) / 1e9,
+                  "hbm_GBps": rate(wbytes_all // 16 * 16, 1) / 1e9}
+        log(args, "probes: " + ", ".join(f"{k} {v:.0f}" for k, v in probes.items()))
+
     # union sizes of this run's tiles/groups (the plan's per-unit counts)
     ntiles = (B + T - 1) // T
     if kernel in (1, 3):
@@ -335,6 +359,10 @@ def main():
             "traffic_source": measured["source"] if measured else None,
             "traffic_frac_of_hbm_peak": (measured["bytes"] / search_s / HBM_PEAK_BPS) if measured else None,
             "algorithmic_bytes": l2_bytes,
+            "measured_peaks": probes,
+            "frac_of_measured_l2": (l2_bytes / search_s / 1e9 / probes["l2_GBps"]) if probes else None,
+            "traffic_frac_of_measured_mall": ((measured["bytes"] / search_s / 1e9 / probes["mall_GBps"])
+                                              if (probes and measured) else None),
             "union_per_doc": union_total / B,
             "alu_useful_adds_frac": useful_adds / search_s / VALU_PEAK_ADDS,
         },

@@ -340,6 +340,20 @@ som_status som_update_finish_f16(uint16_t* W, int64_t F, int64_t ldw, int32_t ro
                                  const uint32_t* acc, int64_t ld_acc, const uint32_t* count, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Measurement aid: read-bandwidth probe.  Reads `bytes` (a multiple of 16) of
+ * device memory at `buf` (16-byte aligned) `passes` times with coalesced
+ * 128-bit loads, every workgroup of an XCD re-reading the same part of the
+ * buffer (so a buffer of a few MB per XCD is served by the L2s after the
+ * first pass, a larger one by the memory-side cache or HBM) and moving to
+ * another CU of that XCD between passes (so the vector L1s do not serve the
+ * re-reads).  `sink` (4 bytes of device memory) is written only for one
+ * value of the folded data; its content is meaningless.  Time the call with
+ * events on `stream`: bytes * passes / time is the read rate.  Nothing is
+ * allocated; buf is never written.
+ * ------------------------------------------------------------------------- */
+som_status som_probe_read(const void* buf, int64_t bytes, int32_t passes, uint32_t* sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -26,6 +26,7 @@ from .som import (  # noqa: F401
     som_codebook_ldw,
     som_codebook_norms,
     som_last_error,
+    som_probe_read,
     som_tile_plan,
     som_update_accumulate,
     som_update_finish,

@@ -20,7 +20,8 @@ OUT = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsom.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "norms.hip", "plan.hip", "search.hip", "search_f16.hip", "cluster.hip", "update.hip"]
+SOURCES = ["api.hip", "norms.hip", "plan.hip", "search.hip", "search_f16.hip", "cluster.hip", "update.hip",
+           "probe.hip"]
 
 # Packed fp32 instructions are switched off for every device compile.
 CFLAGS = [

@@ -284,7 +284,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 10; }
+int32_t som_abi_version(void) { return 11; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -740,6 +740,16 @@ som_status som_update_finish_f16(uint16_t* W, int64_t F, int64_t ldw, int32_t ro
                                  const uint32_t* acc, int64_t ld_acc, const uint32_t* count, void* ws,
                                  size_t ws_bytes, hipStream_t stream) {
   return finish_impl(W, som::kWeightsF16, F, ldw, rows, cols, sigma, acc, ld_acc, count, ws, ws_bytes, stream);
+}
+
+som_status som_probe_read(const void* buf, int64_t bytes, int32_t passes, uint32_t* sink, hipStream_t stream) {
+  if (!buf || !sink) return fail(SOM_ERR_INVALID_ARG, "buf or sink is NULL");
+  if (bytes < 16 || bytes % 16 != 0) return fail(SOM_ERR_INVALID_ARG, "bytes must be a positive multiple of 16");
+  if (!aligned(buf, 16) || !aligned(sink, 4)) return fail(SOM_ERR_INVALID_ARG, "buf must be 16-byte aligned");
+  if (passes < 1) return fail(SOM_ERR_INVALID_ARG, "passes must be >= 1");
+  hipError_t e = som::launch_read_probe(buf, bytes, passes, sink, stream);
+  if (e != hipSuccess) return hip_fail(e, "probe launch");
+  return ok();
 }
 
 }  // extern "C"

@@ -122,6 +122,9 @@ hipError_t launch_update_finish(void* W, int weights, int64_t F, int64_t ldw, in
                                 float* den_tmp, float* den, float* chunk, int64_t chunk_planes,
                                 hipStream_t stream);
 
+// Read-bandwidth probe (probe.hip): `passes` grid-stride reads of buf.
+hipError_t launch_read_probe(const void* buf, int64_t bytes, int32_t passes, uint32_t* sink, hipStream_t stream);
+
 // Clustering.
 size_t cluster_sort_temp_bytes(int64_t B, int64_t F);
 hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,

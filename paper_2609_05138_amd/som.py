@@ -50,6 +50,7 @@ EXPORTS = (
     "som_update_workspace_bytes",
     "som_update_finish",
     "som_update_finish_f16",
+    "som_probe_read",
 )
 
 
@@ -142,6 +143,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     for fn in (lib.som_update_finish, lib.som_update_finish_f16):
         fn.restype = _i32
         fn.argtypes = [_vp, _i64, _i64, _i32, _i32, ctypes.c_double, _vp, _i64, _vp, _vp, _sz, _vp]
+    lib.som_probe_read.restype = _i32
+    lib.som_probe_read.argtypes = [_vp, _i64, _i32, _vp, _vp]
     lib.som_cluster_order.restype = _i32
     lib.som_cluster_order.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _sz, _vp]
     _lib = lib
@@ -510,4 +513,17 @@ def som_bmu_search_unfused(W: torch.Tensor, norms: torch.Tensor, indptr: torch.T
                                       _ptr(perm), _ptr(bmu), _ptr(dist), ctypes.byref(o), int(block_docs), _ptr(ws),
                                       ws.numel(), _stream(stream)))
     return bmu, dist
+
+
+def som_probe_read(buf: torch.Tensor, nbytes: int, passes: int = 1, sink: Optional[torch.Tensor] = None,
+                   stream=None) -> None:
+    """Read-bandwidth probe over the first nbytes of a device tensor (see som.h)."""
+    lib = load()
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous ROCm device tensor")
+    if nbytes > buf.numel() * buf.element_size():
+        raise ValueError("nbytes exceeds the tensor")
+    if sink is None:
+        sink = torch.empty(1, dtype=torch.int32, device=buf.device)
+    _check(lib.som_probe_read(_ptr(buf), int(nbytes), int(passes), _ptr(sink), _stream(stream)))
 

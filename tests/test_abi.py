@@ -42,7 +42,15 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 10
+    assert som.som_abi_version() == 11
+
+
+def test_probe_rejects_bad_arguments(lib):
+    fake = ctypes.c_void_p(0x1000)          # never dereferenced: rejected first
+    for args in ((None, 64, 1, fake), (fake, 64, 1, None), (fake, 8, 1, fake), (fake, 40, 1, fake),
+                 (ctypes.c_void_p(0x1004), 64, 1, fake), (fake, 64, 0, fake)):
+        st, _ = _status(lib, "som_probe_read", *args, None)
+        assert st == som.SOM_ERR_INVALID_ARG, args
 
 
 def test_codebook_ldw_is_host_only(lib):

@@ -384,3 +384,15 @@ def test_planned_search_reuses_a_plan_across_codebooks():
         W64 = W.astype(np.float64)
         _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, a[0].cpu().numpy(),
                     a[1].cpu().numpy(), range(0, 2500, 7))
+
+
+def test_read_probe_runs_and_leaves_the_buffer_alone():
+    """The bandwidth probe only reads: the buffer is unchanged after several
+    passes, at sizes that are not multiples of its workgroup step."""
+    buf = torch.arange(1 << 18, dtype=torch.int32, device=DEV)      # 1 MiB
+    ref = buf.clone()
+    sink = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for nbytes, passes in ((16, 1), (4096 + 16, 3), (1 << 20, 2)):
+        som.som_probe_read(buf, nbytes, passes, sink)
+    torch.cuda.synchronize()
+    assert torch.equal(buf, ref)
