@@ -32,7 +32,7 @@ HBM_PEAK_BPS = 8.0e12
 MEASURED_TRAFFIC = {
     ("map512x512-F20000-2M", 0, 1048576, 262208, "f32", 1,
      '{"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "slice_neurons": 0, "tile_docs": 16}'): {
-        "bytes": 9.6436783e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
+        "bytes": 9.6493747e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
         "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, k_search<float,16,4,1,4,1>, copy-calibrated x2.0 / x1.0",
     },
     ("map512x512-F20000-2M", 0, 1048576, 262208, "f16", 1,
@@ -148,7 +148,7 @@ def main():
     kernel = args.kernel or 1
     # documents that share one sweep of a union: a kernel-1 tile, a kernel-2
     # group or a kernel-3 super-tile
-    T = {1: tile_docs or 8, 2: 64 * (args.group_tiles or 16), 3: tile_docs or 128}[kernel]
+    T = {1: tile_docs or 8, 2: 64 * (args.group_tiles or 16), 3: tile_docs or 64}[kernel]
     cl_ws = torch.empty(max(som.som_cluster_workspace_bytes(B, F, nnz), 1), dtype=torch.uint8, device=dev)
     s_ws = torch.empty(max(som.som_bmu_search_planned_workspace_bytes(N, B, **knobs), 1),
                        dtype=torch.uint8, device=dev)
