@@ -15,11 +15,13 @@
 //                 in LDS: v[r][c] = sum_k g[|k|] t[r+k][c]; then either the
 //                 blurred counts (den) or the write-back W = v / den where
 //                 den > 0 (other units keep their weights)
-//  k_blur_fused   R <= 16: both passes on a 64 x 64 tile (plus halo) in LDS,
-//                 the same sums term for term; the accumulators are read once
-//                 (with the halo) and the codebook written once.
-// Bound: HBM (the two-pass path streams 16 B per element, the fused one
-// about 9-13 B).
+//  k_blur_stream  R <= 16: one wave per 64-column strip of a feature plane
+//                 walks down the rows: row pass from an LDS row buffer,
+//                 column pass from an LDS ring of the last 2R+1 results, the
+//                 same sums term for term; the accumulators are read once and
+//                 the codebook written once.
+// Bound: HBM (the two-pass path streams 16 B per element, the streaming one
+// 8 B plus a halo of 2R/64 of the reads).
 #include "common.h"
 
 namespace som {
@@ -107,72 +109,114 @@ k_blur_cols(const float* __restrict__ t, int64_t ld_t, int rows, int cols, int R
   }
 }
 
-// Fused blur + write-back for small radii: one 64 x 64 tile of one feature
-// per workgroup, loaded with its R-wide halo into LDS (cells outside the grid
-// are zero and add nothing, so the sums equal the two-pass ones term for
-// term); the row pass and the column pass both run in LDS and the codebook
-// is written once.  Grid (tiles, features) with tiles fastest: feature planes
-// sit a power-of-two stride apart, so workgroups that ran the same tile of
-// consecutive features would all hit the same memory channels.
-constexpr int kTile = 64;
-constexpr int kFusedMaxR = 16;
+// Streaming blur + write-back (R <= kStreamMaxR, one instantiation per
+// radius): one wave owns a strip of 64 columns of one feature plane and
+// walks down the grid rows.  Step r loads row r of the strip with its R-wide
+// halo (cells outside the grid are zero) into the wave's own LDS row buffer
+// and forms the row pass t[r][c] = sum_{k=-R..R} g[|k|] acc[r][c+k]; t goes
+// into a ring of the last 2R+1 rows held twice over (slots h and h + 2R+1),
+// so that the column pass of row r - R, sum_{k=-R..R} g[|k|] t[r-R+k][c]
+// (zero rows outside the grid: their slots are still zero), reads 2R+1
+// consecutive slots; then the write-back through the blurred counts.  Both
+// sums take the same terms in the same order as the tile kernels; the taps
+// sit in registers and every LDS read has an immediate offset.  Rows are
+// loaded kStreamAhead steps before use; a wave touches only its own LDS, so
+// there is no workgroup barrier, and every input and output element is read
+// or written once.
+constexpr int kStreamMaxR = 16;
+constexpr int kStreamAhead = 8;
 
-template <typename WT>
-__global__ void __launch_bounds__(256)
-k_blur_fused(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int rows, int cols, int R,
-             const float* __restrict__ g, const float* __restrict__ den, WT* __restrict__ W, int64_t ldw) {
-  extern __shared__ float lds[];
-  const int E = kTile + 2 * R;                    // tile edge with halo
-  float* in = lds;                                // [E][E]
-  float* mid = lds + E * E;                       // [E][kTile]
-  float* taps = mid + E * kTile;                  // [R + 1]
+template <typename WT, int R>
+__global__ void __launch_bounds__(64)
+k_blur_stream(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int rows, int cols,
+              const float* __restrict__ g, const float* __restrict__ den, WT* __restrict__ W, int64_t ldw) {
+  constexpr int H = 2 * R + 1;
+  __shared__ float rb[64 + 2 * R + 1];  // the current row with its halo
+  __shared__ float hist[2 * H][64];     // the last H row-pass results, twice over
+  const int lane = threadIdx.x;
   const int64_t f = f0 + blockIdx.y;
-  const int tiles_x = (cols + kTile - 1) / kTile;
-  const int r0 = (blockIdx.x / tiles_x) * kTile;
-  const int c0 = (blockIdx.x % tiles_x) * kTile;
+  const int c0 = blockIdx.x * 64;
+  const int c = c0 + lane;
   const uint32_t* src = acc + f * ld_acc;
-  for (int i = threadIdx.x; i <= R; i += blockDim.x) taps[i] = g[i];
-  // Thread (ty, tx) loads columns tx and tx + 64 of rows ty, ty + 4, ...: all
-  // of its loads are issued before the first LDS store.
-  constexpr int kMaxE = kTile + 2 * kFusedMaxR;
-  constexpr int kPasses = kMaxE / 4;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  float v[kPasses][2];
+  float tp[R + 1];
 #pragma unroll
-  for (int q = 0; q < kPasses; ++q)
+  for (int i = 0; i <= R; ++i) tp[i] = g[i];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int y = ty + 4 * q, x = tx + 64 * h;
-      const int r = r0 - R + y, c = c0 - R + x;
-      v[q][h] = (y < E && x < E && r >= 0 && r < rows && c >= 0 && c < cols)
-                    ? static_cast<float>(src[static_cast<int64_t>(r) * cols + c])
-                    : 0.f;
-    }
-#pragma unroll
-  for (int q = 0; q < kPasses; ++q)
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int y = ty + 4 * q, x = tx + 64 * h;
-      if (y < E && x < E) in[y * E + x] = v[q][h];
-    }
-  __syncthreads();
-  for (int i = threadIdx.x; i < E * kTile; i += blockDim.x) {
-    const int y = i / kTile, x = i % kTile;
-    const float* row = in + y * E + x;            // taps k = -R..R at row[R + k]
-    float s = 0.f;
-    for (int k = -R; k <= R; ++k) s = fmaf(taps[k < 0 ? -k : k], row[R + k], s);
-    mid[i] = s;
+  for (int i = 0; i < 2 * H; ++i) hist[i][lane] = 0.f;
+  // this lane's two input columns: c0 - R + lane, and c0 - R + 64 + lane for
+  // the halo's last 2R cells
+  const int ca = c0 - R + lane, cb = c0 - R + 64 + lane;
+  const bool va = ca >= 0 && ca < cols, vb = lane < 2 * R && cb >= 0 && cb < cols;
+  float pa[kStreamAhead], pb[kStreamAhead];
+#define SOM_STREAM_LOAD(r, a, b)                                                                    \
+  {                                                                                                \
+    const bool in_ = (r) < rows;                                                                   \
+    a = (in_ && va) ? static_cast<float>(src[static_cast<int64_t>(r) * cols + ca]) : 0.f;          \
+    b = (in_ && vb) ? static_cast<float>(src[static_cast<int64_t>(r) * cols + cb]) : 0.f;          \
   }
-  __syncthreads();
-  for (int i = threadIdx.x; i < kTile * kTile; i += blockDim.x) {
-    const int y = i / kTile, x = i % kTile;
-    const int r = r0 + y, c = c0 + x;
-    if (r >= rows || c >= cols) continue;
-    float s = 0.f;
-    for (int k = -R; k <= R; ++k) s = fmaf(taps[k < 0 ? -k : k], mid[(y + R + k) * kTile + x], s);
-    const int64_t j = static_cast<int64_t>(r) * cols + c;
-    const float dj = den[j];
-    if (dj > 0.f) W[f * ldw + j] = static_cast<WT>(s / dj);
+#pragma unroll
+  for (int u = 0; u < kStreamAhead; ++u) SOM_STREAM_LOAD(u, pa[u], pb[u])
+  const int steps = rows + R;
+  int h = 0;  // slot of row r
+  for (int r0 = 0; r0 < steps; r0 += kStreamAhead) {
+#pragma unroll
+    for (int u = 0; u < kStreamAhead; ++u) {
+      const int r = r0 + u;
+      if (r >= steps) break;
+      const float a = pa[u], b = pb[u];
+      SOM_STREAM_LOAD(r + kStreamAhead, pa[u], pb[u])
+      // row pass of row r (zero beyond the last row)
+      rb[lane] = a;
+      if (lane < 2 * R) rb[64 + lane] = b;
+      __builtin_amdgcn_wave_barrier();
+      float t = 0.f;
+#pragma unroll
+      for (int j = 0; j <= 2 * R; ++j) t = fmaf(tp[j < R ? R - j : j - R], rb[lane + j], t);
+      __builtin_amdgcn_wave_barrier();
+      t = r < rows ? t : 0.f;
+      hist[h][lane] = t;
+      hist[h + H][lane] = t;
+      // column pass of row r - R: slots h+1 .. h+H hold rows r-2R .. r
+      const int ro = r - R;
+      if (ro >= 0) {
+        const int base = h + 1 == H ? 0 : h + 1;
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j <= 2 * R; ++j) s = fmaf(tp[j < R ? R - j : j - R], hist[base + j][lane], s);
+        if (c < cols) {
+          const int64_t jj = static_cast<int64_t>(ro) * cols + c;
+          const float dj = den[jj];
+          if (dj > 0.f) W[f * ldw + jj] = static_cast<WT>(s / dj);
+        }
+      }
+      h = h + 1 == H ? 0 : h + 1;
+    }
+  }
+#undef SOM_STREAM_LOAD
+}
+
+template <typename WT, int R>
+hipError_t launch_stream_r(const uint32_t* acc, int64_t ld_acc, int64_t F, int rows, int cols, const float* taps,
+                           const float* den, WT* W, int64_t ldw, hipStream_t stream) {
+  const uint32_t strips64 = static_cast<uint32_t>((cols + 63) / 64);
+  for (int64_t f0 = 0; f0 < F; f0 += 65535) {  // grid.y holds at most 65535 features
+    const uint32_t fc = static_cast<uint32_t>(F - f0 < 65535 ? F - f0 : 65535);
+    hipLaunchKernelGGL((k_blur_stream<WT, R>), dim3(strips64, fc), dim3(64), 0, stream, acc, ld_acc, f0, rows, cols,
+                       taps, den, W, ldw);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <typename WT, int R = 0>
+hipError_t launch_stream(int r, const uint32_t* acc, int64_t ld_acc, int64_t F, int rows, int cols, const float* taps,
+                         const float* den, WT* W, int64_t ldw, hipStream_t stream) {
+  if constexpr (R > kStreamMaxR) {
+    return hipErrorInvalidValue;
+  } else {
+    if (r == R) return launch_stream_r<WT, R>(acc, ld_acc, F, rows, cols, taps, den, W, ldw, stream);
+    return launch_stream<WT, R + 1>(r, acc, ld_acc, F, rows, cols, taps, den, W, ldw, stream);
   }
 }
 
@@ -218,27 +262,11 @@ hipError_t launch_update_finish(void* W, int weights, int64_t F, int64_t ldw, in
                      N, den_tmp, N, cols, R, taps);
   hipLaunchKernelGGL((k_blur_cols<float, 0>), dim3(strips, 1), dim3(256), col_lds, stream, den_tmp, N, rows, cols, R,
                      taps, den, nullptr, nullptr, int64_t(0));
-  if (R <= kFusedMaxR) {
-    // numerators blurred tile by tile in LDS and written back through den
-    const int E = kTile + 2 * R;
-    const size_t lds = sizeof(float) * (static_cast<size_t>(E) * E + static_cast<size_t>(E) * kTile + R + 1);
-    const auto fused = weights == kWeightsF16 ? reinterpret_cast<const void*>(&k_blur_fused<_Float16>)
-                                              : reinterpret_cast<const void*>(&k_blur_fused<float>);
-    hipError_t e = hipFuncSetAttribute(fused, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-    if (e != hipSuccess) return e;
-    const uint32_t tiles = static_cast<uint32_t>(((rows + kTile - 1) / kTile) * ((cols + kTile - 1) / kTile));
-    for (int64_t f0 = 0; f0 < F; f0 += 65535) {  // grid.y holds at most 65535 features
-      const uint32_t fc = static_cast<uint32_t>(F - f0 < 65535 ? F - f0 : 65535);
-      if (weights == kWeightsF16)
-        hipLaunchKernelGGL(k_blur_fused<_Float16>, dim3(tiles, fc), dim3(256), lds, stream, acc, ld_acc, f0, rows,
-                           cols, R, taps, den, static_cast<_Float16*>(W), ldw);
-      else
-        hipLaunchKernelGGL(k_blur_fused<float>, dim3(tiles, fc), dim3(256), lds, stream, acc, ld_acc, f0, rows, cols,
-                           R, taps, den, static_cast<float*>(W), ldw);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
-    return hipGetLastError();
+  if (R <= kStreamMaxR) {
+    // numerators streamed down 64-column strips, written back through den
+    if (weights == kWeightsF16)
+      return launch_stream<_Float16>(R, acc, ld_acc, F, rows, cols, taps, den, static_cast<_Float16*>(W), ldw, stream);
+    return launch_stream<float>(R, acc, ld_acc, F, rows, cols, taps, den, static_cast<float*>(W), ldw, stream);
   }
   // larger radii: numerators a chunk of features at a time, row pass into the
   // chunk buffer, then the column pass written back through den

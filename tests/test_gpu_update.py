@@ -104,7 +104,8 @@ def test_sigma_zero_is_the_exact_mean(rows, cols):
 
 
 @pytest.mark.parametrize("rows,cols,sigma", [(4, 5, 0.5), (16, 16, 1.0), (1, 37, 2.5), (33, 8, 2.5),
-                                             (12, 12, 7.3), (9, 20, 0.2)])
+                                             (12, 12, 7.3), (9, 20, 0.2), (20, 130, 2.0), (70, 67, 5.3),
+                                             (5, 200, 1.7)])
 def test_blur_matches_oracle(rows, cols, sigma):
     rng = np.random.default_rng(int(sigma * 10) + rows)
     F, N = 40, rows * cols
