@@ -113,16 +113,17 @@ k_blur_cols(const float* __restrict__ t, int64_t ld_t, int rows, int cols, int R
 // radius): one wave owns a strip of 64 columns of one feature plane and
 // walks down the grid rows.  Step r loads row r of the strip with its R-wide
 // halo (cells outside the grid are zero) into the wave's own LDS row buffer
-// and forms the row pass t[r][c] = sum_{k=-R..R} g[|k|] acc[r][c+k]; t goes
-// into a ring of the last 2R+1 rows held twice over (slots h and h + 2R+1),
-// so that the column pass of row r - R, sum_{k=-R..R} g[|k|] t[r-R+k][c]
-// (zero rows outside the grid: their slots are still zero), reads 2R+1
-// consecutive slots; then the write-back through the blurred counts.  Both
-// sums take the same terms in the same order as the tile kernels; the taps
-// sit in registers and every LDS read has an immediate offset.  Rows are
-// loaded kStreamAhead steps before use; a wave touches only its own LDS, so
-// there is no workgroup barrier, and every input and output element is read
-// or written once.
+// and forms the row pass t[r][c] = sum_{k=-R..R} g[|k|] acc[r][c+k]; each
+// lane keeps the row-pass results of the last 2R+1 rows in registers (the
+// step loop is unrolled by a multiple of 2R+1, so a row's slot is a static
+// index), from which the column pass of row r - R,
+// sum_{k=-R..R} g[|k|] t[r-R+k][c] (zero rows outside the grid: their slots
+// still hold zero), is formed; then the write-back through the blurred
+// counts.  Both sums take the same terms in the same order as the two-pass
+// kernels; the taps sit in registers and every LDS read has an immediate
+// offset.  Rows are loaded at least kStreamAhead steps before use; a wave
+// touches only its own LDS, so there is no workgroup barrier, and every input
+// and output element is read or written once.
 constexpr int kStreamMaxR = 16;
 constexpr int kStreamAhead = 8;
 
@@ -131,8 +132,10 @@ __global__ void __launch_bounds__(64)
 k_blur_stream(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int rows, int cols,
               const float* __restrict__ g, const float* __restrict__ den, WT* __restrict__ W, int64_t ldw) {
   constexpr int H = 2 * R + 1;
+  // steps per unrolled block: a multiple of H (so row r's history slot is
+  // the static index (r mod H)), and at least kStreamAhead (the prefetch depth)
+  constexpr int U = H * ((kStreamAhead + H - 1) / H);
   __shared__ float rb[64 + 2 * R + 1];  // the current row with its halo
-  __shared__ float hist[2 * H][64];     // the last H row-pass results, twice over
   const int lane = threadIdx.x;
   const int64_t f = f0 + blockIdx.y;
   const int c0 = blockIdx.x * 64;
@@ -141,13 +144,14 @@ k_blur_stream(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int 
   float tp[R + 1];
 #pragma unroll
   for (int i = 0; i <= R; ++i) tp[i] = g[i];
+  float hr[H];  // row-pass results of the last H rows: row r in slot r mod H
 #pragma unroll
-  for (int i = 0; i < 2 * H; ++i) hist[i][lane] = 0.f;
+  for (int i = 0; i < H; ++i) hr[i] = 0.f;
   // this lane's two input columns: c0 - R + lane, and c0 - R + 64 + lane for
   // the halo's last 2R cells
   const int ca = c0 - R + lane, cb = c0 - R + 64 + lane;
   const bool va = ca >= 0 && ca < cols, vb = lane < 2 * R && cb >= 0 && cb < cols;
-  float pa[kStreamAhead], pb[kStreamAhead];
+  float pa[U], pb[U];
 #define SOM_STREAM_LOAD(r, a, b)                                                                    \
   {                                                                                                \
     const bool in_ = (r) < rows;                                                                   \
@@ -155,16 +159,15 @@ k_blur_stream(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int 
     b = (in_ && vb) ? static_cast<float>(src[static_cast<int64_t>(r) * cols + cb]) : 0.f;          \
   }
 #pragma unroll
-  for (int u = 0; u < kStreamAhead; ++u) SOM_STREAM_LOAD(u, pa[u], pb[u])
+  for (int u = 0; u < U; ++u) SOM_STREAM_LOAD(u, pa[u], pb[u])
   const int steps = rows + R;
-  int h = 0;  // slot of row r
-  for (int r0 = 0; r0 < steps; r0 += kStreamAhead) {
+  for (int r0 = 0; r0 < steps; r0 += U) {
 #pragma unroll
-    for (int u = 0; u < kStreamAhead; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int r = r0 + u;
       if (r >= steps) break;
       const float a = pa[u], b = pb[u];
-      SOM_STREAM_LOAD(r + kStreamAhead, pa[u], pb[u])
+      SOM_STREAM_LOAD(r + U, pa[u], pb[u])
       // row pass of row r (zero beyond the last row)
       rb[lane] = a;
       if (lane < 2 * R) rb[64 + lane] = b;
@@ -173,23 +176,19 @@ k_blur_stream(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int 
 #pragma unroll
       for (int j = 0; j <= 2 * R; ++j) t = fmaf(tp[j < R ? R - j : j - R], rb[lane + j], t);
       __builtin_amdgcn_wave_barrier();
-      t = r < rows ? t : 0.f;
-      hist[h][lane] = t;
-      hist[h + H][lane] = t;
-      // column pass of row r - R: slots h+1 .. h+H hold rows r-2R .. r
-      const int ro = r - R;
-      if (ro >= 0) {
-        const int base = h + 1 == H ? 0 : h + 1;
+      hr[u % H] = r < rows ? t : 0.f;
+      // column pass of row r - R: slots (u+1 .. u+H) mod H hold rows r-2R .. r
+      // (slots of rows before the first still hold zero)
+      if (r >= R) {
         float s = 0.f;
 #pragma unroll
-        for (int j = 0; j <= 2 * R; ++j) s = fmaf(tp[j < R ? R - j : j - R], hist[base + j][lane], s);
+        for (int j = 0; j <= 2 * R; ++j) s = fmaf(tp[j < R ? R - j : j - R], hr[(u + 1 + j) % H], s);
         if (c < cols) {
-          const int64_t jj = static_cast<int64_t>(ro) * cols + c;
+          const int64_t jj = static_cast<int64_t>(r - R) * cols + c;
           const float dj = den[jj];
           if (dj > 0.f) W[f * ldw + jj] = static_cast<WT>(s / dj);
         }
       }
-      h = h + 1 == H ? 0 : h + 1;
     }
   }
 #undef SOM_STREAM_LOAD
