@@ -209,13 +209,15 @@ __device__ __forceinline__ void epilogue(const SearchArgs& a, const float (&acc)
       const int64_t j = n0 + 64 * E * q + E * lane + e;
       nrm[E * q + e] = j < a.N ? a.norms[j] : 0.f;
     }
+  // one loop per output form (the choice is wave-uniform), each small enough
+  // to unroll fully, so the accumulators stay in registers
+  if (a.score) {  // unfused comparator: write the distances, no argmin here
 #pragma unroll
-  for (int s = 0; s < T; ++s) {
-    const int64_t p = p0 + s;
-    if (p >= a.B) break;
-    const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
-    const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
-    if (a.score) {  // unfused comparator: write the distances, no argmin here
+    for (int s = 0; s < T; ++s) {
+      const int64_t p = p0 + s;
+      if (p >= a.B) break;
+      const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
+      const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
       float* row = a.score + (p - a.tile_base * T) * a.N;
 #pragma unroll
       for (int q = 0; q < Q; ++q)
@@ -224,9 +226,16 @@ __device__ __forceinline__ void epilogue(const SearchArgs& a, const float (&acc)
           const int64_t j = n0 + 64 * E * q + E * lane + e;
           if (j < a.N) row[j] = fmaf(-2.f, acc[s][E * q + e], nnz + nrm[E * q + e]);
         }
-      continue;
     }
-    if (a.keys2) {  // best and second best (wave-uniform branch)
+    return;
+  }
+  if (a.keys2) {  // best and second best
+#pragma unroll
+    for (int s = 0; s < T; ++s) {
+      const int64_t p = p0 + s;
+      if (p >= a.B) break;
+      const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
+      const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
       uint64_t k1 = kNoKey, k2 = kNoKey;
 #pragma unroll
       for (int q = 0; q < Q; ++q)
@@ -239,8 +248,15 @@ __device__ __forceinline__ void epilogue(const SearchArgs& a, const float (&acc)
         }
       wave_top2_u64(k1, k2);
       if (lane == 0) top2_merge(a.keys + p, a.keys2 + p, k1, k2);
-      continue;
     }
+    return;
+  }
+#pragma unroll
+  for (int s = 0; s < T; ++s) {
+    const int64_t p = p0 + s;
+    if (p >= a.B) break;
+    const int64_t d = a.perm ? static_cast<int64_t>(a.perm[p]) : p;
+    const float nnz = static_cast<float>(a.indptr[d + 1] - a.indptr[d]);
     float best = 0.f;
     uint32_t bj = 0xffffffffu;
 #pragma unroll
