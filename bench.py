@@ -322,6 +322,17 @@ def main():
                          f"(single-threaded numpy) against all {N} neurons in {el:.1f}s; "
                          f"its fp64 norms pass ({oracle_norm_s:.1f}s) excluded"}
 
+    l2_rate = l2_bytes / search_s
+    levels = {"l2_algorithmic_vs_derived_peak": l2_rate / L2_PEAK_BPS}
+    if probes:
+        levels["l2_algorithmic_vs_measured_l2"] = l2_rate / (probes["l2_GBps"] * 1e9)
+    if measured:
+        fab = measured["bytes"] / search_s
+        levels["fabric_measured_vs_hbm_peak"] = fab / HBM_PEAK_BPS
+        if probes:
+            levels["fabric_measured_vs_measured_mall"] = fab / (probes["mall_GBps"] * 1e9)
+    levels["binding"] = max((k for k in levels if k != "binding"), key=lambda k: levels[k])
+
     out = {
         "metric": "doc-neuron pairs scored/sec",
         "value": value,
@@ -360,6 +371,9 @@ def main():
             "traffic_frac_of_hbm_peak": (measured["bytes"] / search_s / HBM_PEAK_BPS) if measured else None,
             "algorithmic_bytes": l2_bytes,
             "measured_peaks": probes,
+            # every level against its roof (the survey's protocol names the
+            # binding level as the one at the highest fraction)
+            "levels": levels,
             "frac_of_measured_l2": (l2_bytes / search_s / 1e9 / probes["l2_GBps"]) if probes else None,
             "traffic_frac_of_measured_mall": ((measured["bytes"] / search_s / 1e9 / probes["mall_GBps"])
                                               if (probes and measured) else None),
