@@ -69,7 +69,8 @@ typedef enum som_status {
  *   documents (tile_docs: 64, 128 or 256) against 256 neurons (fp32) or 512
  *   (fp16); the super-tile's union (Section 4.1 with a tile of D documents)
  *   is fetched once per workgroup with 128-bit loads into LDS, and each wave
- *   (16 documents for fp32, 8 for fp16) adds the rows its documents hold.
+ *   (8 documents; 16 for D = 256 with an fp32 codebook) adds the rows its
+ *   documents hold.
  *   Its plan is the tile plan with D-document tiles; a plan built with the
  *   same tile_docs serves both storage types.
  * Every kernel cuts the neuron axis into slices whose minima are merged

@@ -110,7 +110,8 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
     p->D = T;
     p->nchunks = (N + 64 * K - 1) / (64 * K);
   } else if (kernel == 3) {
-    // super-tile of D documents; waves of 16 (fp32) or 8 (fp16) documents
+    // super-tile of D documents; waves of 8 documents (16 for D = 256 with an
+    // fp32 codebook, as a workgroup holds at most 16 waves)
     if (o.group_tiles || o.mask_mode || o.slice_neurons)
       return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles, mask_mode and slice_neurons must be 0 for kernel 3");
     const int D = o.tile_docs ? o.tile_docs : 64;
@@ -120,7 +121,7 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
     const int K = f16 ? 8 : 4;
     if (o.lane_neurons && o.lane_neurons != K)
       return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0 (or 4 for fp32, 8 for fp16) for kernel 3");
-    p->T = f16 ? 8 : 16;
+    p->T = D == 256 ? 16 : 8;
     p->K = K;
     p->group = D / p->T;
     p->mask_mode = 1;

@@ -268,13 +268,18 @@ hipError_t launch_k1(const SearchArgs& a, hipStream_t stream) {
 
 hipError_t launch_k3(const SearchArgs& a, hipStream_t stream) {
   if (a.weights == kWeightsF16) return launch_search_st_f16(a, stream);
-  if (a.T != 16 || a.K != 4) return hipErrorInvalidValue;
-  switch (a.group) {
-    case 4: return launch_st<float, 16, 4, 4>(a, stream);
-    case 8: return launch_st<float, 16, 4, 8>(a, stream);
-    case 16: return launch_st<float, 16, 4, 16>(a, stream);
-    default: return hipErrorInvalidValue;
+  if (a.K != 4) return hipErrorInvalidValue;
+  // waves of 8 documents for 64- and 128-document super-tiles, of 16 for 256
+  // (a workgroup holds at most 16 waves)
+  if (a.T == 8) {
+    switch (a.group) {
+      case 8: return launch_st<float, 8, 4, 8>(a, stream);
+      case 16: return launch_st<float, 8, 4, 16>(a, stream);
+      default: return hipErrorInvalidValue;
+    }
   }
+  if (a.T == 16 && a.group == 16) return launch_st<float, 16, 4, 16>(a, stream);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_search(const SearchArgs& a, hipStream_t stream) {

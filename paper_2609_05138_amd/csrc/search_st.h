@@ -206,11 +206,12 @@ k_search_st(SearchArgs a) {
 
 template <typename WT, int T, int K, int S>
 hipError_t launch_st(const SearchArgs& a, hipStream_t stream) {
-  // 16-entry stages in a ring of two: 32 KB of rows per workgroup, so up to
-  // five workgroups share a CU.  Measured on the 512^2 map (fp32, 262,144
-  // documents): the number of workgroups per CU decides the speed (each
-  // stage ends in a barrier that waits for the wave with the most rows);
-  // 32-entry stages and deeper rings (1 to 2 workgroups per CU) were slower.
+  // 16-entry stages in a ring of two: 32 KB of rows per workgroup, so four
+  // workgroups of eight 8-document waves share a CU.  Measured on the 512^2
+  // map (fp32, 262,144 documents): the number of waves a CU can interleave
+  // decides the speed (each stage ends in a barrier that waits for the wave
+  // with the most rows, and a wave's adds form a serial chain); 32-entry
+  // stages, deeper rings and 16-document waves were slower.
   constexpr int P = 16;
   constexpr int NSLOT = 2;
   const dim3 grid(static_cast<uint32_t>((a.ntiles + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));

@@ -185,7 +185,7 @@ def test_f16_planned_search_shares_the_fp32_plan():
     assert torch.equal(n32, n16)
     ref = None
     for knobs in (dict(), dict(kernel=3), dict(kernel=3, tile_docs=128)):
-        # kernel 3: 16-document waves for fp32, 8 for fp16, the same super-tile plan
+        # kernel 3: the same super-tile plan for both storage types
         plan = som.som_plan(ip, ix, 20000, **knobs)
         a = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W32d, n32, ip, plan, N=2048)]
         b = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W16d, n16, ip, plan, N=2048)]
