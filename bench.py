@@ -138,14 +138,18 @@ def main():
     bmu2 = torch.empty(B, dtype=torch.int32, device=dev) if args.top2 else None
     dist2 = torch.empty(B, dtype=torch.float32, device=dev) if args.top2 else None
     perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
-    # launch configuration: the library's defaults, except 16-document tiles for
-    # an fp32 codebook (measured 5% faster on the 512^2 map; fp16 keeps 8)
-    tile_docs = args.tile_docs or (8 if args.weights == "f16" or args.kernel == 2 else 16)
-    if args.kernel in (2, 3):
+    # launch configuration: kernel 1 with the library's defaults, except
+    # 16-document tiles for an fp32 codebook (measured 5% faster on the 512^2
+    # map; fp16 keeps 8); for the topic workload (no global head, unions 1.5x
+    # larger) kernel 3 with 64-document shared-union super-tiles (measured 17%
+    # faster there, 6% slower on the 512^2 Zipf batch)
+    kernel_arg = args.kernel or (3 if (args.config == 5 and args.weights == "f32" and not args.unfused) else 0)
+    tile_docs = args.tile_docs or (8 if args.weights == "f16" or kernel_arg == 2 else 16)
+    if kernel_arg in (2, 3):
         tile_docs = args.tile_docs
-    knobs = dict(kernel=args.kernel, tile_docs=tile_docs, lane_neurons=args.lane_neurons,
+    knobs = dict(kernel=kernel_arg, tile_docs=tile_docs, lane_neurons=args.lane_neurons,
                  group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons)
-    kernel = args.kernel or 1
+    kernel = kernel_arg or 1
     # documents that share one sweep of a union: a kernel-1 tile, a kernel-2
     # group or a kernel-3 super-tile
     T = {1: tile_docs or 8, 2: 64 * (args.group_tiles or 16), 3: tile_docs or 64}[kernel]

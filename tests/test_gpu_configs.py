@@ -2,9 +2,10 @@
 
 For the 256^2 and 512^2 maps (N = 65,536 and 262,144 neurons, F = 20,000,
 codebooks of 5.2 and 21 GB) the oracle cannot score a whole batch, so each
-test runs the device search on a full batch in the launch configuration the
-benchmark uses (kernel 1, 16-document tiles for fp32 and 8 for fp16, codebook
-rows at the recommended stride) and checks:
+test runs the device search on a full batch in the launch configurations the
+benchmark uses (kernel 1, 16-document tiles for fp32 and 8 for fp16; kernel 3
+with 64-document super-tiles, the benchmark's choice for the topic workload;
+codebook rows at the recommended stride) and checks:
   * that the shared-union super-tile kernel (kernel 3) returns bit-identical
     results on the whole batch,
   * a seeded sample of documents (always including the first and the last)
