@@ -35,6 +35,11 @@ MEASURED_TRAFFIC = {
         "bytes": 9.6432781e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
         "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, k_search<float,16,4,1,4,1>, copy-calibrated x2.0 / x1.0",
     },
+    ("map512x512-F20000-26.9M-topics", 0, 1000000, 262208, "f32", 3,
+     '{"group_tiles": 0, "kernel": 3, "lane_neurons": 0, "mask_mode": 0, "slice_neurons": 0, "tile_docs": 0}'): {
+        "bytes": 1.87804e10 * 1024 * 2.0 + 3.2e7 * 1024 * 1.0,
+        "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, k_search_st<float,8,4,8,16,2>, copy-calibrated x2.0 / x1.0",
+    },
     ("map512x512-F20000-2M", 0, 1048576, 262208, "f16", 1,
      '{"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "slice_neurons": 0, "tile_docs": 8}'): {
         "bytes": 4.8041349e9 * 1024 * 2.0 + 1.6777216e7 * 1024 * 1.0,
@@ -140,10 +145,11 @@ def main():
     perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
     # launch configuration: kernel 1 with the library's defaults, except
     # 16-document tiles for an fp32 codebook (measured 5% faster on the 512^2
-    # map; fp16 keeps 8); for the topic workload (no global head, unions 1.5x
-    # larger) kernel 3 with 64-document shared-union super-tiles (measured 17%
-    # faster there, 6% slower on the 512^2 Zipf batch)
-    kernel_arg = args.kernel or (3 if (args.config == 5 and args.weights == "f32" and not args.unfused) else 0)
+    # map; fp16 keeps 8); for the 128^2 map and the topic workload (no global
+    # head, unions 1.5x larger) kernel 3 with 64-document shared-union
+    # super-tiles (measured 15% and 17% faster there, 6-7% slower on the
+    # 256^2 and 512^2 Zipf batches)
+    kernel_arg = args.kernel or (3 if (args.config in (2, 5) and args.weights == "f32" and not args.unfused) else 0)
     tile_docs = args.tile_docs or (8 if args.weights == "f16" or kernel_arg == 2 else 16)
     if kernel_arg in (2, 3):
         tile_docs = args.tile_docs

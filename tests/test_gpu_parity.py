@@ -263,6 +263,11 @@ def test_config2_first_batch():
     indptr, indices = documents(2, 0)                   # 65,536 documents
     B = len(indptr) - 1
     bmu, dist, _ = _search(W, indptr, indices, ldw=som.som_codebook_ldw(W.shape[1]))
+    # the benchmark's launch configuration for this map (kernel 3, 64-document
+    # super-tiles, clustered): bit-identical on the whole batch
+    perm = oracle.cluster_order(indptr, indices, W.shape[0])
+    b3, d3, _ = _search(W, indptr, indices, ldw=som.som_codebook_ldw(W.shape[1]), perm=perm, kernel=3)
+    assert np.array_equal(b3, bmu) and np.array_equal(d3, dist)
     W64 = W.astype(np.float64)
     norms64 = oracle.codebook_norms(W64)
     rng = np.random.default_rng(0)
