@@ -167,7 +167,9 @@ som_status som_bmu_search_top2(const float* W, int64_t F, int64_t N, int64_t ldw
  *   som_plan            builds the plan into `plan` (device memory of at least
  *                       som_plan_bytes(B, nnz, opts) bytes, 256-byte aligned)
  *   som_bmu_search_planned  searches with it; indptr, perm and opts must be those
- *                       the plan was built with; ws holds the per-document
+ *                       the plan was built with, and F at least som_plan's (the
+ *                       plan's feature ids index codebook rows unchecked); ws
+ *                       holds the per-document
  *                       packed minima, best and second best
  *                       (som_bmu_search_planned_workspace_bytes, 16 B per
  *                       document) */

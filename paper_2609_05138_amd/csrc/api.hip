@@ -2,6 +2,7 @@
 // workspace carving and kernel sequencing.  No entry point allocates device
 // memory; every array comes from the caller.
 #include <cmath>
+#include <cstdint>
 #include <string>
 
 #include "../../include/som.h"
@@ -46,6 +47,8 @@ som_status check_codebook(const void* W, int weights, int64_t F, int64_t N, int6
   if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
   if (N < 1 || N > kI32Max) return fail(SOM_ERR_INVALID_ARG, "N must be in [1, 2^31)");
   if (ldw < N) return fail(SOM_ERR_INVALID_ARG, "ldw must be >= N");
+  // row offsets f * ldw are formed in 64-bit byte arithmetic on the device
+  if (ldw > (INT64_MAX / 4) / F) return fail(SOM_ERR_INVALID_ARG, "F * ldw exceeds the addressable range");
   if (weights == som::kWeightsF16 && ldw % 8 != 0)
     return fail(SOM_ERR_INVALID_ARG, "ldw must be a multiple of 8 for an fp16 codebook");
   if (ldw % 4 != 0) return fail(SOM_ERR_INVALID_ARG, "ldw must be a multiple of 4");

@@ -130,6 +130,7 @@ def test_search_rejects_bad_arguments(lib):
     assert call(B=-1)[0] == som.SOM_ERR_INVALID_ARG
     assert call(nnz=-1)[0] == som.SOM_ERR_INVALID_ARG
     assert call(ldw=6)[0] == som.SOM_ERR_INVALID_ARG
+    assert call(F=1 << 30, ldw=1 << 40)[0] == som.SOM_ERR_INVALID_ARG   # F * ldw beyond 64-bit byte offsets
     st, msg = call(ws_bytes=16)
     assert st == som.SOM_ERR_WORKSPACE and "need" in msg
     assert call(ws=null)[0] == som.SOM_ERR_WORKSPACE
