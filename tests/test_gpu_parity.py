@@ -344,6 +344,58 @@ def test_single_neuron_and_long_documents():
     _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, bmu, dist, range(40))
 
 
+def test_largest_neuron_count_of_one_launch():
+    # one launch takes at most 65,535 neuron slices (the grid's second
+    # dimension): 256-neuron slices give N = 65,535 * 256.  Neurons planted
+    # equal to a document (distance exactly 0) in the last slice and in the
+    # first must be found; an exact tie across slices goes to the lower index.
+    rng = np.random.default_rng(17)
+    F, NMAX = 8, 65535 * 256
+    ldw = NMAX + 64
+    W = np.zeros((F, ldw), np.float32)
+    W[:, :NMAX + 1] = rng.random((F, NMAX + 1), dtype=np.float32) * 0.5 + 0.25
+    docs = _random_docs(rng, 40, F, mean=3, empty_every=13)
+    docs[1], docs[2], docs[3] = [0, 3, 5], [1, 2, 7], [4, 6]
+    plant = {1: [NMAX - 1], 2: [NMAX - 300], 3: [70000, 5]}   # doc -> neurons equal to it
+    for d, js in plant.items():
+        x = np.zeros(F, np.float32)
+        x[docs[d]] = 1.0
+        for j in js:
+            W[:, j] = x
+    indptr, indices = _csr(docs)
+    W64 = W.astype(np.float64)
+    norms64 = oracle.codebook_norms(W64, NMAX)
+    Wd = torch.from_numpy(W).to(DEV)
+    norms = som.som_codebook_norms(Wd, N=NMAX)
+    ip, ix = _dev_i32(indptr), _dev_i32(indices)
+    first = None
+    for knobs in (dict(), dict(kernel=1, tile_docs=16), dict(kernel=1, lane_neurons=8), dict(kernel=3)):
+        bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=NMAX, **knobs)
+        torch.cuda.synchronize()
+        b, dd = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
+        assert (b[1], b[2], b[3]) == (NMAX - 1, NMAX - 300, 5), (knobs, b[1:4])
+        assert np.all(dd[1:4] == 0.0)
+        if first is None:   # the oracle once; every launch form sums in the same order
+            _check_docs(W64, norms64, indptr, indices, b, dd, range(len(docs)), N=NMAX)
+            first = (b, dd)
+        else:
+            assert np.array_equal(b, first[0]) and np.array_equal(dd, first[1]), knobs
+    # one neuron more needs a 65,536th slice at 256 neurons per slice (and
+    # kernel 2's 32-neuron slices run out long before)
+    norms1 = som.som_codebook_norms(Wd, N=NMAX + 1)
+    for N, knobs in ((NMAX + 1, dict()), (NMAX + 1, dict(kernel=3)), (NMAX, dict(kernel=2))):
+        with pytest.raises(som.SomError) as e:
+            som.som_bmu_search(Wd, norms1[:N], ip, ix, N=N, **knobs)
+        assert e.value.status == 1 and "slices" in str(e.value)
+    # 512-neuron slices still fit: N = NMAX + 1 with 8 neurons per lane
+    bmu, dist = som.som_bmu_search(Wd, norms1, ip, ix, N=NMAX + 1, kernel=1, lane_neurons=8)
+    torch.cuda.synchronize()
+    b = bmu.cpu().numpy().astype(np.int64)
+    assert (b[1], b[2], b[3]) == (NMAX - 1, NMAX - 300, 5)
+    _check_docs(W64, oracle.codebook_norms(W64, NMAX + 1), indptr, indices, b,
+                dist.cpu().numpy().astype(np.float64), range(len(docs)), N=NMAX + 1)
+
+
 def test_validate_rejects_malformed_batches():
     rng = np.random.default_rng(11)
     W = rng.random((50, 64), dtype=np.float32)
