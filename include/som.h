@@ -137,7 +137,13 @@ size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
  *           evaluated in fp32 (dot summed in ascending feature order)
  *   ws      device workspace of at least som_bmu_workspace_bytes(...) bytes,
  *           256-byte aligned
- * B == 0 is a valid no-op. */
+ * B == 0 is a valid no-op.  One call is one launch, which takes at most
+ * 65,535 neuron slices (N <= 65,535 * 64 * K: 16,776,960 neurons at the fp32
+ * default of 4 per lane; kernel 2 slices are opts->slice_neurons wide) and
+ * fewer than 2^24 tiles or groups (ceil(B / T)); larger sizes return
+ * SOM_ERR_INVALID_ARG: split the batch, or the neuron axis (searching
+ * column ranges of W and keeping each document's smaller distance, the
+ * earlier range's on a tie). */
 som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
                           const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
                           const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,

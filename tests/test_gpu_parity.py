@@ -396,6 +396,46 @@ def test_largest_neuron_count_of_one_launch():
                 dist.cpu().numpy().astype(np.float64), range(len(docs)), N=NMAX + 1)
 
 
+def test_largest_tile_count_of_one_launch():
+    # one launch takes fewer than 2^24 tiles: with one-document tiles the
+    # largest batch is 2^24 - 1 documents (most of them empty here, so the
+    # test stays small), and one more is rejected until the tiles grow
+    rng = np.random.default_rng(19)
+    F, N, B = 50, 300, (1 << 24) - 1
+    W = rng.random((F, N), dtype=np.float32)
+    lens = np.zeros(B + 1, np.int64)
+    full = np.sort(rng.choice(B + 1, 400, replace=False))
+    lens[full] = rng.integers(1, 12, full.size)
+    docs = {int(d): np.sort(rng.choice(F, int(lens[d]), replace=False)) for d in full}
+    indptr = np.zeros(B + 2, np.int64)
+    indptr[1:] = np.cumsum(lens)
+    indices = np.concatenate([docs[int(d)] for d in full])
+    W64 = W.astype(np.float64)
+    norms64 = oracle.codebook_norms(W64)
+    Wd, ld = _dev_W(W)
+    norms = som.som_codebook_norms(Wd, N=N)
+    ipB = _dev_i32(indptr[:B + 1])
+    nnzB = int(indptr[B])
+    ixB = _dev_i32(indices[:nnzB])
+    bmu, dist = som.som_bmu_search(Wd, norms, ipB, ixB, N=N, tile_docs=1)
+    torch.cuda.synchronize()
+    b, dd = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
+    empty = lens[:B] == 0
+    e0 = int(np.flatnonzero(empty)[0])
+    _check_docs(W64, norms64, indptr, indices, b, dd, [e0] + [int(d) for d in full if d < B], N=N)
+    assert np.all(b[empty] == b[e0]) and np.all(dd[empty] == dd[e0])
+    # 2^24 documents: too many one-document tiles, fine as two-document tiles
+    ip1, ix1 = _dev_i32(indptr), _dev_i32(indices)
+    with pytest.raises(som.SomError) as e:
+        som.som_bmu_search(Wd, norms, ip1, ix1, N=N, tile_docs=1)
+    assert e.value.status == 1 and "too many tiles" in str(e.value)
+    bmu2, dist2 = som.som_bmu_search(Wd, norms, ip1, ix1, N=N, tile_docs=2)
+    torch.cuda.synchronize()
+    b2, d2 = bmu2.cpu().numpy().astype(np.int64), dist2.cpu().numpy().astype(np.float64)
+    assert np.array_equal(b2[:B], b) and np.array_equal(d2[:B], dd)
+    _check_docs(W64, norms64, indptr, indices, b2, d2, [B], N=N)
+
+
 def test_validate_rejects_malformed_batches():
     rng = np.random.default_rng(11)
     W = rng.random((50, 64), dtype=np.float32)
