@@ -141,9 +141,13 @@ size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
  * 65,535 neuron slices (N <= 65,535 * 64 * K: 16,776,960 neurons at the fp32
  * default of 4 per lane; kernel 2 slices are opts->slice_neurons wide) and
  * fewer than 2^24 tiles or groups (ceil(B / T)); larger sizes return
- * SOM_ERR_INVALID_ARG: split the batch, or the neuron axis (searching
- * column ranges of W and keeping each document's smaller distance, the
- * earlier range's on a tie). */
+ * SOM_ERR_INVALID_ARG: split the batch, or the neuron axis.  A column range
+ * [r0, r0 + n) of W is searched as W + r0 and norms + r0 with the same ldw
+ * and N = n (r0 a multiple of 4, of 8 for fp16); as a row's padding may be
+ * read up to ldw elements from its start, the buffer must stay readable for
+ * r0 elements after its last row.  Adding r0 to bmu and keeping each
+ * document's smaller distance, the earlier range's on a tie, gives the
+ * whole search's bmu and dist exactly. */
 som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
                           const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
                           const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,

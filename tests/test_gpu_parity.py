@@ -436,6 +436,62 @@ def test_largest_tile_count_of_one_launch():
     _check_docs(W64, norms64, indptr, indices, b2, d2, [B], N=N)
 
 
+def test_neuron_ranges_compose_to_the_full_search():
+    # The neuron-sharded form on one GPU: each column range of W is searched
+    # through the C ABI at a pointer offset into the same feature-major rows
+    # (same ldw, the norms at the same offset); keeping each document's smaller
+    # distance, the earlier range's on a tie, gives the whole-map search bit for
+    # bit, exact ties across ranges included.
+    import ctypes
+    from paper_2609_05138_amd import som as abi
+    rng = np.random.default_rng(23)
+    F, N = 300, 1000
+    W = rng.random((F, N), dtype=np.float32)
+    docs = _random_docs(rng, 700, F, mean=12, empty_every=97)
+    for d, cols in ((5, (100, 700)), (6, (3, 950)), (7, (255, 256))):   # planted exact ties
+        x = np.zeros(F, np.float32)
+        x[docs[d]] = 1.0
+        for j in cols:
+            W[:, j] = x
+    W[:, 604] = W[:, 603]                                               # a tie at a range edge
+    indptr, indices = _csr(docs)
+    B = len(docs)
+    # a range at offset r0 may read each row's padding up to ldw elements from
+    # W + r0, so the buffer keeps ldw elements of slack after its last row
+    ldw = 1024
+    buf = torch.zeros(F * ldw + ldw, dtype=torch.float32, device=DEV)
+    Wd = buf[:F * ldw].view(F, ldw)
+    Wd[:, :N] = torch.from_numpy(W).to(DEV)
+    norms = som.som_codebook_norms(Wd, N=N)
+    ip, ix = _dev_i32(indptr), _dev_i32(indices)
+    lib = som.load()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for knobs in (dict(), dict(kernel=1, tile_docs=16), dict(kernel=3)):
+        full_b, full_d = som.som_bmu_search(Wd, norms, ip, ix, N=N, **knobs)
+        best_b = np.full(B, -1, np.int64)
+        best_d = np.full(B, np.inf, np.float32)
+        for r0, r1 in ((0, 256), (256, 604), (604, N)):                 # offsets keep 16-byte rows
+            n = r1 - r0
+            o = abi.som_bmu_opts(int(knobs.get("kernel", 0)), int(knobs.get("tile_docs", 0)), 0, 0, 0, 0, 0, 0)
+            need = int(lib.som_bmu_workspace_bytes(F, n, B, len(indices), ctypes.byref(o)))
+            ws = torch.empty(max(need, 1), dtype=torch.uint8, device=DEV)
+            bmu = torch.empty(B, dtype=torch.int32, device=DEV)
+            dist = torch.empty(B, dtype=torch.float32, device=DEV)
+            st = lib.som_bmu_search(Wd.data_ptr() + 4 * r0, F, n, ldw, norms.data_ptr() + 4 * r0, ip.data_ptr(),
+                                    ix.data_ptr(), B, len(indices), None, bmu.data_ptr(), dist.data_ptr(),
+                                    ctypes.byref(o), ws.data_ptr(), ws.numel(), stream)
+            assert st == abi.SOM_OK, lib.som_last_error()
+            torch.cuda.synchronize()
+            b = bmu.cpu().numpy().astype(np.int64) + r0
+            dd = dist.cpu().numpy()
+            take = dd < best_d                                           # strict: the earlier range keeps ties
+            best_b[take], best_d[take] = b[take], dd[take]
+        torch.cuda.synchronize()
+        assert np.array_equal(best_b, full_b.cpu().numpy().astype(np.int64)), knobs
+        assert np.array_equal(best_d, full_d.cpu().numpy()), knobs
+        assert (best_b[5], best_b[6], best_b[7]) == (100, 3, 255)
+
+
 def test_validate_rejects_malformed_batches():
     rng = np.random.default_rng(11)
     W = rng.random((50, 64), dtype=np.float32)
