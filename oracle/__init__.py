@@ -27,4 +27,5 @@ from .update import (  # noqa: F401
     neighbourhood_radius,
     update_accumulate,
     update_finish,
+    update_finish_at,
 )

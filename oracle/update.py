@@ -18,13 +18,16 @@ states a reading, the textbook batch map:
     wherever that denominator is positive; a neuron whose neighbourhood
     caught no document keeps its weights.
 
-Everything is a direct evaluation in fp64 with a dense [N, N] neighbourhood
-matrix (small maps only).  Pins (tests/test_oracle_update.py): sigma = 0
+Everything is a direct evaluation in fp64: update_finish with a dense [N, N]
+neighbourhood matrix (small maps only), update_finish_at with the window sums
+of the definition at listed units (any map size).  Pins (tests/test_oracle_update.py): sigma = 0
 gives each unit the mean of its documents; one document moves every unit of
 its neighbourhood exactly onto itself; the dense matrix equals the product of
 two one-dimensional Gaussians (separability) and is symmetric; the update is
 linear in the accumulators (two batches accumulated = one batch of both);
-document order does not matter.
+document order does not matter; update_finish_at equals update_finish on
+small maps, and on a 512 x 512 map reproduces the one-document and sigma = 0
+closed forms.
 """
 
 from __future__ import annotations
@@ -80,3 +83,30 @@ def update_finish(W: np.ndarray, acc: np.ndarray, count: np.ndarray, rows: int, 
     moved = den > 0
     new[:, moved] = num[:, moved] / den[moved]
     return new
+
+
+def update_finish_at(W_at: np.ndarray, acc: np.ndarray, count: np.ndarray, rows: int, cols: int,
+                     sigma: float, units) -> np.ndarray:
+    """New weights at the listed units only, for maps too large for the dense matrix.
+
+    W_at [F', len(units)] holds the old weights there, acc [F', N] the
+    accumulators of the same F' features, count [N] the unit counts.  For unit
+    j the window sums of the definition are evaluated term by term:
+    num = sum over units i with |dr| <= R and |dc| <= R of h(i, j) acc[:, i],
+    den likewise over count; the unit moves to num / den when den > 0.
+    """
+    R = neighbourhood_radius(sigma)
+    out = np.array(W_at, dtype=np.float64)
+    for k, j in enumerate(units):
+        r, c = divmod(int(j), cols)
+        num = np.zeros(acc.shape[0], np.float64)
+        den = 0.0
+        for rr in range(max(0, r - R), min(rows, r + R + 1)):
+            for cc in range(max(0, c - R), min(cols, c + R + 1)):
+                i = rr * cols + cc
+                h = 1.0 if sigma <= 0 else math.exp(-((rr - r) ** 2 + (cc - c) ** 2) / (2.0 * sigma * sigma))
+                num += h * acc[:, i].astype(np.float64)
+                den += h * float(count[i])
+        if den > 0:
+            out[:, k] = num / den
+    return out

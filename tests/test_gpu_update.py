@@ -93,13 +93,13 @@ def test_sigma_zero_is_the_exact_mean(rows, cols):
     acc, cnt = _accumulate([(docs, bmu)], F, N)
     W = rng.random((F, N)).astype(np.float32)
     got = _finish(W, acc, cnt, rows, cols, 0.0)
-    a = acc.cpu().numpy().astype(np.float32)
-    c = cnt.cpu().numpy().astype(np.float32)
+    oa, oc = oracle.update_accumulate(*_csr(docs), bmu, F, N)
+    a, c = oa.astype(np.float32), oc.astype(np.float32)   # exact: counts are far below 2^24
     want = W.copy()
     moved = c > 0
     want[:, moved] = a[:, moved] / c[moved]               # IEEE fp32 division of exact integers
     assert np.array_equal(got, want)
-    ref = oracle.update_finish(W.astype(np.float64), *oracle.update_accumulate(*_csr(docs), bmu, F, N), rows, cols, 0.0)
+    ref = oracle.update_finish(W.astype(np.float64), oa, oc, rows, cols, 0.0)
     assert np.array_equal(got, ref.astype(np.float32))
 
 
@@ -146,19 +146,67 @@ def test_many_feature_chunks_and_a_large_radius():
     docs, bmu = _batch(rng, 20000, F, N, mean=60)
     acc, cnt = _accumulate([(docs, bmu)], F, N)
     W = rng.random((F, N)).astype(np.float32)
+    # the oracle's own accumulators: the device's must equal them exactly
+    oa, oc = oracle.update_accumulate(*_csr(docs), bmu, F, N)
+    assert np.array_equal(acc.cpu().numpy().astype(np.int64), oa)
+    assert np.array_equal(cnt.cpu().numpy().astype(np.int64), oc)
     got0 = _finish(W, acc, cnt, rows, cols, 0.0)
-    a = acc.cpu().numpy()
-    c = cnt.cpu().numpy().astype(np.float32)
+    c = oc.astype(np.float32)
     moved = c > 0
     want0 = W.copy()
-    want0[:, moved] = a[:, moved].astype(np.float32) / c[moved]
+    want0[:, moved] = oa[:, moved].astype(np.float32) / c[moved]    # exact integers, one IEEE division
     assert np.array_equal(got0, want0)
     sigma = 9.0
     got = _finish(W, acc, cnt, rows, cols, sigma).astype(np.float64)
     sample = np.unique(np.concatenate([[0, planes - 1, planes, 2 * planes, F - 1], rng.choice(F, 25, replace=False)]))
-    ref = oracle.update_finish(W[sample].astype(np.float64), a[sample].astype(np.int64), cnt.cpu().numpy().astype(np.int64),
-                               rows, cols, sigma)
+    ref = oracle.update_finish(W[sample].astype(np.float64), oa[sample], oc, rows, cols, sigma)
     R = oracle.neighbourhood_radius(sigma)
     tol = (4 * (2 * R + 1) + 4) * U
     assert np.all(np.abs(got[sample] - ref) <= tol * np.abs(ref) + 1e-30)
     assert math.isfinite(float(got.sum()))
+
+
+def test_full_size_update_on_the_512_map():
+    """The benchmark's update configuration, on sampled outputs: a 512 x 512
+    map, F = 20,000, one 1,048,576-document batch of the 512^2 workload and
+    sigma = 2 (R = 6).  The assignments are seeded inputs (not search
+    results).  The oracle accumulates the sampled features only (the scatter
+    is independent per feature) and evaluates the window sums at sampled
+    units, borders and corners included."""
+    from synth import documents
+    rows = cols = 512
+    N, F, sigma = rows * cols, 20000, 2.0
+    indptr, indices = documents(4, 0)
+    B = len(indptr) - 1
+    rng = np.random.default_rng(31)
+    bmu = rng.integers(0, N, B)
+    ldw = som.som_codebook_ldw(N)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(7)
+    W = torch.rand((F, ldw), generator=gen, device=DEV)
+    feats = np.unique(np.concatenate([[0, 1, 9, 99, 999, F - 1], rng.choice(F, 10, replace=False)]))
+    fidx = torch.from_numpy(feats).to(DEV)
+    old = W[fidx].cpu().numpy()                         # this test's own input, before the update
+    acc = torch.zeros((F, N), dtype=torch.int32, device=DEV)
+    cnt = torch.zeros(N, dtype=torch.int32, device=DEV)
+    som.som_update_accumulate(_i32(indptr), _i32(indices), _i32(bmu), F, N, acc, cnt)
+    som.som_update_finish(W, rows, cols, sigma, acc, cnt)
+    torch.cuda.synchronize()
+    got_acc = acc[fidx].cpu().numpy().astype(np.int64)
+    got_cnt = cnt.cpu().numpy().astype(np.int64)
+    new = W[fidx].cpu().numpy().astype(np.float64)
+    del acc, W
+    torch.cuda.empty_cache()
+    keep = np.isin(indices, feats)
+    docid = np.repeat(np.arange(B), np.diff(indptr))
+    ip_f = np.zeros(B + 1, np.int64)
+    ip_f[1:] = np.cumsum(np.bincount(docid[keep], minlength=B))
+    ix_f = np.searchsorted(feats, indices[keep])
+    oa, oc = oracle.update_accumulate(ip_f, ix_f, bmu, len(feats), N)
+    assert np.array_equal(got_acc, oa) and np.array_equal(got_cnt, oc)
+    edge = [0, 1, cols - 1, N - cols, N - 1, 5 * cols, 8 * cols - 2, N - 4, 256 * cols + 256]
+    units = np.unique(np.concatenate([edge, rng.choice(N, 120, replace=False)]))
+    ref = oracle.update_finish_at(old[:, units].astype(np.float64), oa, oc, rows, cols, sigma, units)
+    R = oracle.neighbourhood_radius(sigma)
+    tol = (4 * (2 * R + 1) + 4) * U
+    assert np.all(np.abs(new[:, units] - ref) <= tol * np.abs(ref) + 1e-30)

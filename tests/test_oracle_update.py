@@ -119,3 +119,43 @@ def test_update_equals_the_weighted_mean_written_out():
             assert np.allclose(new[:, j], (wts[:, None] * X).sum(axis=0) / wts.sum(), rtol=1e-13, atol=1e-15)
         else:
             assert np.array_equal(new[:, j], W[:, j])
+
+
+@pytest.mark.parametrize("rows,cols,sigma", [(6, 7, 0.0), (6, 7, 0.8), (9, 5, 1.7), (1, 40, 2.5), (12, 12, 3.1)])
+def test_pointwise_finish_equals_the_dense_one(rows, cols, sigma):
+    # every unit, borders included (truncated windows)
+    rng = np.random.default_rng(int(sigma * 10) + rows)
+    F, N = 20, rows * cols
+    docs, bmu = _random(rng, 120, F, max(1, N - 5))
+    W = rng.random((F, N))
+    acc, cnt = oracle.update_accumulate(*_csr(docs), bmu, F, N)
+    dense = oracle.update_finish(W, acc, cnt, rows, cols, sigma)
+    units = np.arange(N)
+    at = oracle.update_finish_at(W[:, units], acc, cnt, rows, cols, sigma, units)
+    assert np.allclose(at, dense, rtol=1e-12, atol=0.0)
+
+
+def test_pointwise_finish_closed_forms_on_a_512_map():
+    # one document moves exactly the units of its window onto itself; with
+    # sigma = 0 a unit becomes the mean of its documents
+    rows = cols = 512
+    N = rows * cols
+    F = 6
+    x = [1, 4]
+    b = 3 * cols + 500                                   # near a corner: a clipped window
+    acc, cnt = oracle.update_accumulate(*_csr([x]), np.array([b]), F, N)
+    W = np.full((F, 5), 0.25)
+    units = np.array([b, b - 2 * cols + 3, b + 6 * cols, b + 7 * cols, 0])   # in, in, in (R = 6), out, out
+    got = oracle.update_finish_at(W, acc, cnt, rows, cols, 2.0, units)
+    want = np.zeros(F)
+    want[x] = 1.0
+    for k in range(3):
+        assert np.array_equal(got[:, k], want)
+    assert np.array_equal(got[:, 3:], W[:, 3:])
+    docs = [[0, 2], [2, 5], [1]]
+    bm = np.array([77, 77, 9000])
+    acc, cnt = oracle.update_accumulate(*_csr(docs), bm, F, N)
+    got = oracle.update_finish_at(np.zeros((F, 3)), acc, cnt, rows, cols, 0.0, [77, 9000, 78])
+    assert np.array_equal(got[:, 0], np.array([0.5, 0, 1.0, 0, 0, 0.5]))
+    assert np.array_equal(got[:, 1], np.array([0, 1.0, 0, 0, 0, 0]))
+    assert np.array_equal(got[:, 2], np.zeros(F))
