@@ -121,7 +121,8 @@ k_blur_cols(const float* __restrict__ t, int64_t ld_t, int rows, int cols, int R
 // still hold zero), is formed; then the write-back through the blurred
 // counts.  Both sums take the same terms in the same order as the two-pass
 // kernels; the taps sit in registers and every LDS read has an immediate
-// offset.  Rows are loaded at least kStreamAhead steps before use; a wave
+// offset.  Rows, and the blurred counts of the rows written back, are loaded
+// at least kStreamAhead steps before use; a wave
 // touches only its own LDS, so there is no workgroup barrier, and every input
 // and output element is read or written once.
 constexpr int kStreamMaxR = 16;
@@ -151,23 +152,35 @@ k_blur_stream(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int 
   // the halo's last 2R cells
   const int ca = c0 - R + lane, cb = c0 - R + 64 + lane;
   const bool va = ca >= 0 && ca < cols, vb = lane < 2 * R && cb >= 0 && cb < cols;
-  float pa[U], pb[U];
-#define SOM_STREAM_LOAD(r, a, b)                                                                    \
+  // Raw words in flight, with the blurred count of the row written back at
+  // the step that uses them (row r - R): every lane loads unconditionally
+  // (cells outside the grid read element 0 instead), and the selects and the
+  // conversion happen when the row is used, so no load is waited for in the
+  // step that issues it.
+  const bool vc = c < cols;
+  uint32_t pa[U], pb[U];
+  float pd[U];
+#define SOM_STREAM_LOAD(r, a, b, d)                                                                 \
   {                                                                                                \
     const bool in_ = (r) < rows;                                                                   \
-    a = (in_ && va) ? static_cast<float>(src[static_cast<int64_t>(r) * cols + ca]) : 0.f;          \
-    b = (in_ && vb) ? static_cast<float>(src[static_cast<int64_t>(r) * cols + cb]) : 0.f;          \
+    const int rd_ = (r) - R;                                                                       \
+    a = src[(in_ && va) ? static_cast<int64_t>(r) * cols + ca : 0];                                \
+    b = src[(in_ && vb) ? static_cast<int64_t>(r) * cols + cb : 0];                                \
+    d = den[(rd_ >= 0 && rd_ < rows && vc) ? static_cast<int64_t>(rd_) * cols + c : 0];            \
   }
 #pragma unroll
-  for (int u = 0; u < U; ++u) SOM_STREAM_LOAD(u, pa[u], pb[u])
+  for (int u = 0; u < U; ++u) SOM_STREAM_LOAD(u, pa[u], pb[u], pd[u])
   const int steps = rows + R;
   for (int r0 = 0; r0 < steps; r0 += U) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = r0 + u;
       if (r >= steps) break;
-      const float a = pa[u], b = pb[u];
-      SOM_STREAM_LOAD(r + U, pa[u], pb[u])
+      const bool in = r < rows;
+      const float a = (in && va) ? static_cast<float>(pa[u]) : 0.f;
+      const float b = (in && vb) ? static_cast<float>(pb[u]) : 0.f;
+      const float dj = pd[u];  // blurred count of row r - R (read only when r >= R and c < cols)
+      SOM_STREAM_LOAD(r + U, pa[u], pb[u], pd[u])
       // row pass of row r (zero beyond the last row)
       rb[lane] = a;
       if (lane < 2 * R) rb[64 + lane] = b;
@@ -183,11 +196,7 @@ k_blur_stream(const uint32_t* __restrict__ acc, int64_t ld_acc, int64_t f0, int 
         float s = 0.f;
 #pragma unroll
         for (int j = 0; j <= 2 * R; ++j) s = fmaf(tp[j < R ? R - j : j - R], hr[(u + 1 + j) % H], s);
-        if (c < cols) {
-          const int64_t jj = static_cast<int64_t>(r - R) * cols + c;
-          const float dj = den[jj];
-          if (dj > 0.f) W[f * ldw + jj] = static_cast<WT>(s / dj);
-        }
+        if (vc && dj > 0.f) W[f * ldw + static_cast<int64_t>(r - R) * cols + c] = static_cast<WT>(s / dj);
       }
     }
   }
