@@ -251,6 +251,8 @@ def _search(top2, W, norms, indptr, indices, N, perm, validate, outs, ws, stream
     _dev(indices, torch.int32, "indices")
     F, ldw = W.shape
     n = ldw if N is None else int(N)
+    if norms.numel() < n:
+        raise ValueError("norms must hold at least N values")
     B = indptr.numel() - 1
     nnz = indices.numel()
     if perm is not None:
@@ -338,6 +340,8 @@ def _planned(top2, W, norms, indptr, plan, N, outs, ws, stream):
     _dev(indptr, torch.int32, "indptr")
     F, ldw = W.shape
     n = ldw if N is None else int(N)
+    if norms.numel() < n:
+        raise ValueError("norms must hold at least N values")
     B = indptr.numel() - 1
     if B != plan.B:
         raise ValueError("plan was built for another batch")
@@ -499,6 +503,8 @@ def som_bmu_search_unfused(W: torch.Tensor, norms: torch.Tensor, indptr: torch.T
     _dev(indices, torch.int32, "indices")
     F, ldw = W.shape
     n = ldw if N is None else int(N)
+    if norms.numel() < n:
+        raise ValueError("norms must hold at least N values")
     B = indptr.numel() - 1
     nnz = indices.numel()
     if perm is not None:
