@@ -492,6 +492,27 @@ def test_neuron_ranges_compose_to_the_full_search():
         assert (best_b[5], best_b[6], best_b[7]) == (100, 3, 255)
 
 
+def test_binding_rejects_short_norms():
+    # the C ABI cannot size device buffers: the binding checks norms against N
+    rng = np.random.default_rng(29)
+    W = rng.random((40, 96), dtype=np.float32)
+    Wd, _ = _dev_W(W)
+    norms = som.som_codebook_norms(Wd, N=90)
+    ip, ix = _dev_i32(np.array([0, 2, 3])), _dev_i32(np.array([1, 7, 5]))
+    with pytest.raises(ValueError):
+        som.som_bmu_search(Wd, norms, ip, ix)               # N defaults to ldw = 96
+    with pytest.raises(ValueError):
+        som.som_bmu_search_top2(Wd, norms, ip, ix, N=91)
+    plan = som.som_plan(ip, ix, 40)
+    with pytest.raises(ValueError):
+        som.som_bmu_search_planned(Wd, norms, ip, plan, N=96)
+    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=90)
+    torch.cuda.synchronize()
+    W64 = W.astype(np.float64)
+    _check_docs(W64, oracle.codebook_norms(W64, 90), np.array([0, 2, 3]), np.array([1, 7, 5]),
+                bmu.cpu().numpy(), dist.cpu().numpy(), range(2), N=90)
+
+
 def test_validate_rejects_malformed_batches():
     rng = np.random.default_rng(11)
     W = rng.random((50, 64), dtype=np.float32)
