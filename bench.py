@@ -32,8 +32,8 @@ HBM_PEAK_BPS = 8.0e12
 MEASURED_TRAFFIC = {
     ("map512x512-F20000-2M", 0, 1048576, 262208, "f32", 1,
      '{"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "slice_neurons": 0, "tile_docs": 16}'): {
-        "bytes": 9.6432781e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
-        "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, k_search<float,16,4,1,4,1>, copy-calibrated x2.0 / x1.0",
+        "bytes": 9.6514549e9 * 1024 * 2.0 + 3.3554432e7 * 1024 * 1.0,
+        "source": "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE, k_search<float,16,4,1,2,1>, copy-calibrated x2.0 / x1.0",
     },
     ("map512x512-F20000-26.9M-topics", 0, 1000000, 262208, "f32", 3,
      '{"group_tiles": 0, "kernel": 3, "lane_neurons": 0, "mask_mode": 0, "slice_neurons": 0, "tile_docs": 0}'): {
