@@ -3,9 +3,12 @@
 For the 256^2 and 512^2 maps (N = 65,536 and 262,144 neurons, F = 20,000,
 codebooks of 5.2 and 21 GB) the oracle cannot score a whole batch, so each
 test runs the device search on a full batch in the launch configurations the
-benchmark uses (kernel 1, 16-document tiles for fp32 and 8 for fp16; kernel 3
-with 64-document super-tiles, the benchmark's choice for the topic workload;
+benchmark uses (kernel 1, 16-document tiles for fp32, four tiles per
+workgroup on the 512^2 map, and 8-document tiles for fp16; kernel 3 with
+64-document super-tiles, the benchmark's choice for the topic workload;
 codebook rows at the recommended stride) and checks:
+  * that kernel 1 with one tile per workgroup returns bit-identical results
+    where the benchmark groups four,
   * that the shared-union super-tile kernel (kernel 3) returns bit-identical
     results on the whole batch,
   * a seeded sample of documents (always including the first and the last)
@@ -32,7 +35,7 @@ else:  # collected on CPU-only machines, never run there
 REL = 1e-5
 
 
-def _run(cfg_key, batch, cluster, sample, seed, top2=False, f16=False):
+def _run(cfg_key, batch, cluster, sample, seed, top2=False, f16=False, group_tiles=0):
     from synth import CONFIGS, codebook, documents
     cfg = CONFIGS[cfg_key]
     dev = torch.device("cuda:0")
@@ -49,7 +52,11 @@ def _run(cfg_key, batch, cluster, sample, seed, top2=False, f16=False):
     ix = torch.from_numpy(indices).to(dev)
     norms = som.som_codebook_norms(Wd, N=cfg.N)
     perm = som.som_cluster_order(ip, ix, cfg.F) if cluster else None
-    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm, tile_docs=16)
+    bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm, tile_docs=16, group_tiles=group_tiles)
+    if group_tiles > 1:  # a workgroup's tiles are independent: same results ungrouped
+        b1, d1 = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm, tile_docs=16)
+        assert torch.equal(b1, bmu) and torch.equal(d1, dist), "grouped tiles differ from single tiles"
+        del b1, d1
     # the shared-union super-tile kernel sums every dot product in the same
     # order: bit-identical results on the whole batch
     b3, d3 = som.som_bmu_search(Wd, norms, ip, ix, N=cfg.N, perm=perm, kernel=3)
@@ -125,11 +132,11 @@ def test_config3_map256_first_batch():
 
 
 def test_config4_map512_first_batch():
-    _run(4, 0, cluster=False, sample=300, seed=4, top2=True, f16=True)
+    _run(4, 0, cluster=False, sample=300, seed=4, top2=True, f16=True, group_tiles=4)
 
 
 def test_config4_map512_ragged_last_batch():
-    _run(4, 1, cluster=True, sample=150, seed=41)
+    _run(4, 1, cluster=True, sample=150, seed=41, group_tiles=4)
 
 
 def test_config5_topics_clustered_last_batch():
