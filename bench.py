@@ -92,7 +92,7 @@ def log(args, *a):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
 
     import torch
@@ -386,8 +386,8 @@ def main():
             "traffic_frac_of_hbm_peak": (measured["bytes"] / search_s / HBM_PEAK_BPS) if measured else None,
             "algorithmic_bytes": l2_bytes,
             "measured_peaks": probes,
-            # every level against its roof (the survey's protocol names the
-            # binding level as the one at the highest fraction)
+            # every level against its roof; the binding level is the one at
+            # the highest fraction
             "levels": levels,
             "frac_of_measured_l2": (l2_bytes / search_s / 1e9 / probes["l2_GBps"]) if probes else None,
             "traffic_frac_of_measured_mall": ((measured["bytes"] / search_s / 1e9 / probes["mall_GBps"])
