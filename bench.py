@@ -48,7 +48,7 @@ MEASURED_TRAFFIC = {
 }
 
 
-def parse():
+def parse(argv=None):
     p = argparse.ArgumentParser(description=__doc__)
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=3)
@@ -81,12 +81,34 @@ def parse():
     p.add_argument("--quiet", action="store_true")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run a device-to-device copy of MIB MiB (for scaling traffic counters)")
-    return p.parse_args()
+    return p.parse_args(argv)
 
 
 def log(args, *a):
     if not args.quiet:
         print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def launch_knobs(args):
+    """(kernel option, tile_docs, search knobs) of the timed launch."""
+    # launch configuration: kernel 1 with the library's defaults, except
+    # 16-document tiles for an fp32 codebook (measured 5% faster on the 512^2
+    # map; fp16 keeps 8); for the 128^2 map and the topic workload (no global
+    # head, unions 1.5x larger) kernel 3 with 64-document shared-union
+    # super-tiles (measured 15% and 17% faster there, 6-7% slower on the
+    # 256^2 and 512^2 Zipf batches)
+    kernel_arg = args.kernel or (3 if (args.config in (2, 5) and args.weights == "f32" and not args.unfused) else 0)
+    tile_docs = args.tile_docs or (8 if args.weights == "f16" or kernel_arg == 2 else 16)
+    if kernel_arg in (2, 3):
+        tile_docs = args.tile_docs
+    # four 16-document tiles per workgroup on the 512^2 Zipf map in fp32
+    # (measured 2.9% faster per 1M-document batch; neutral or slower on the
+    # 256^2 map and in fp16)
+    group_tiles = args.group_tiles or (4 if (args.config == 4 and args.weights == "f32" and kernel_arg in (0, 1)
+                                             and tile_docs == 16) else 0)
+    knobs = dict(kernel=kernel_arg, tile_docs=tile_docs, lane_neurons=args.lane_neurons,
+                 group_tiles=group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons)
+    return kernel_arg, tile_docs, knobs
 
 
 def main():
@@ -143,23 +165,7 @@ def main():
     bmu2 = torch.empty(B, dtype=torch.int32, device=dev) if args.top2 else None
     dist2 = torch.empty(B, dtype=torch.float32, device=dev) if args.top2 else None
     perm = None if args.no_cluster else torch.empty(B, dtype=torch.int32, device=dev)
-    # launch configuration: kernel 1 with the library's defaults, except
-    # 16-document tiles for an fp32 codebook (measured 5% faster on the 512^2
-    # map; fp16 keeps 8); for the 128^2 map and the topic workload (no global
-    # head, unions 1.5x larger) kernel 3 with 64-document shared-union
-    # super-tiles (measured 15% and 17% faster there, 6-7% slower on the
-    # 256^2 and 512^2 Zipf batches)
-    kernel_arg = args.kernel or (3 if (args.config in (2, 5) and args.weights == "f32" and not args.unfused) else 0)
-    tile_docs = args.tile_docs or (8 if args.weights == "f16" or kernel_arg == 2 else 16)
-    if kernel_arg in (2, 3):
-        tile_docs = args.tile_docs
-    # four 16-document tiles per workgroup on the 512^2 Zipf map in fp32
-    # (measured 2.9% faster per 1M-document batch; neutral or slower on the
-    # 256^2 map and in fp16)
-    group_tiles = args.group_tiles or (4 if (args.config == 4 and args.weights == "f32" and kernel_arg in (0, 1)
-                                             and tile_docs == 16) else 0)
-    knobs = dict(kernel=kernel_arg, tile_docs=tile_docs, lane_neurons=args.lane_neurons,
-                 group_tiles=group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons)
+    kernel_arg, tile_docs, knobs = launch_knobs(args)
     kernel = kernel_arg or 1
     # documents that share one sweep of a union: a kernel-1 tile, a kernel-2
     # group or a kernel-3 super-tile

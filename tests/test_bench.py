@@ -36,3 +36,23 @@ def test_help_lists_the_contract_flags():
     assert r.returncode == 0
     for flag in ("--gpus", "--steps", "--warmup", "--config", "--weights", "--update"):
         assert flag in r.stdout
+
+
+def test_default_launches_match_their_counter_entries():
+    # the fabric-traffic figure is reported only when the timed launch is the
+    # one the counters were taken on; a change of launch knobs must come with
+    # new counters, not with a silently missing figure
+    sys.path.insert(0, ROOT)
+    import bench
+    from synth import CONFIGS, batch_sizes
+    for argv, cfg_key, weights in ((["--config", "4"], 4, "f32"), (["--weights", "f16"], 4, "f16"),
+                                   (["--config", "5"], 5, "f32")):
+        args = bench.parse(argv)
+        kernel_arg, _, knobs = bench.launch_knobs(args)
+        cfg = CONFIGS[cfg_key]
+        keys = [k for k in bench.MEASURED_TRAFFIC if k[0] == cfg.name and k[4] == weights]
+        assert keys, argv
+        for k in keys:
+            assert k[1] == 0 and k[2] == batch_sizes(cfg)[0], argv
+            assert k[5] == (kernel_arg or 1), argv
+            assert k[6] == json.dumps(knobs, sort_keys=True), argv
