@@ -57,6 +57,14 @@ typedef enum som_status {
  * is summed in ascending feature order whatever the knobs, so outputs are
  * bit-identical across all settings.
  *
+ * Automatic choices (measured on the 512^2 and 256^2 maps, F = 20,000,
+ * 1M-document batches): kernel 1; tiles of 16 documents for an fp32
+ * codebook and 8 for fp16; four tiles per workgroup for fp32 tiles of 16
+ * documents when N >= 131,072, one otherwise.  The automatic tile size
+ * depends on the storage type: a search that plans internally uses its own
+ * (fp32 or fp16); som_plan, som_plan_bytes and the planned searches use
+ * opts->storage, so a plan and its search always agree on the geometry.
+ *
  * kernel 1, neurons on lanes: a wave holds a tile of T documents (Section
  *   4.1) against 64*K neurons (K per lane, 128-bit loads, Section 4.3) and
  *   sweeps the tile's union once, adding each row into the documents whose
@@ -78,16 +86,18 @@ typedef enum som_status {
 typedef struct som_bmu_opts {
   int32_t kernel;        /* 0 = auto (kernel 1), 1 = neurons on lanes, 2 = documents on lanes,
                             3 = shared-union super-tiles */
-  int32_t tile_docs;     /* kernel 1: T = 0 (auto: 8), 1, 2, 4, 8, 16 or 32;
+  int32_t tile_docs;     /* kernel 1: T = 0 (auto: 16 for fp32, 8 for fp16), 1, 2, 4, 8, 16 or 32;
                             kernel 3: D = 0 (auto: 64), 64, 128 or 256 (256: fp32 only) */
-  int32_t lane_neurons;  /* kernel 1: K = 0 (auto: 4), 4 or 8; T = 32 needs 4 */
-  int32_t group_tiles;   /* kernel 1: tiles per workgroup, 0 (auto), 1, 2, 4 or 8;
+  int32_t lane_neurons;  /* kernel 1: K = 0 (auto: 4 for fp32, 8 for fp16), 4 or 8; T = 32 needs 4 */
+  int32_t group_tiles;   /* kernel 1: tiles per workgroup, 0 (auto: see above), 1, 2, 4 or 8;
                             kernel 2: waves per workgroup G, 0 (auto), 4, 8 or 16 */
   int32_t mask_mode;     /* kernel 1: 0 = auto, 1 = branch-free multiply by the membership
                             bit, 2 = one scalar branch per document; kernel 3: 0 */
   int32_t slice_neurons; /* kernel 2: NB = 0 (auto), 32 or 64 */
   int32_t validate;      /* 1 = check the CSR batch on the device first (synchronises `stream`) */
-  int32_t reserved;      /* must be 0 */
+  int32_t storage;       /* 0 = fp32, 1 = fp16: the codebook storage type whose automatic tile
+                            size som_plan, som_plan_bytes and the planned searches resolve
+                            (searches that plan internally use their own type) */
 } som_bmu_opts;
 
 /* Version of this ABI (bumped on any incompatible change). */
@@ -117,8 +127,9 @@ som_status som_codebook_norms(const float* W, int64_t F, int64_t N, int64_t ldw,
  * a layout choice for speed only.  Returns 0 for N < 1. */
 int64_t som_codebook_ldw(int64_t N);
 
-/* Bytes of device workspace som_bmu_search needs for these sizes and
- * options (0 if the arguments are invalid). */
+/* Bytes of device workspace som_bmu_search (or som_bmu_search_f16) needs
+ * for these sizes and options (0 if the arguments are invalid); with
+ * automatic tile sizes it covers both storage types. */
 size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
                                const som_bmu_opts* opts);
 
@@ -141,13 +152,12 @@ size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
  * 65,535 neuron slices (N <= 65,535 * 64 * K: 16,776,960 neurons at the fp32
  * default of 4 per lane; kernel 2 slices are opts->slice_neurons wide) and
  * fewer than 2^24 tiles or groups (ceil(B / T)); larger sizes return
- * SOM_ERR_INVALID_ARG: split the batch, or the neuron axis.  A column range
+ * SOM_ERR_INVALID_ARG: split the batch, or the neuron axis.  No row is read
+ * beyond its first round_up(N, 4) elements (8 for fp16), so a column range
  * [r0, r0 + n) of W is searched as W + r0 and norms + r0 with the same ldw
- * and N = n (r0 a multiple of 4, of 8 for fp16); as a row's padding may be
- * read up to ldw elements from its start, the buffer must stay readable for
- * r0 elements after its last row.  Adding r0 to bmu and keeping each
- * document's smaller distance, the earlier range's on a tie, gives the
- * whole search's bmu and dist exactly. */
+ * and N = n (r0 a multiple of 4, of 8 for fp16).  Adding r0 to bmu and
+ * keeping each document's smaller distance, the earlier range's on a tie,
+ * gives the whole search's bmu and dist exactly. */
 som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
                           const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
                           const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,

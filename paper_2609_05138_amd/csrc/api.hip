@@ -64,8 +64,8 @@ som_status check_batch(const int32_t* indptr, const int32_t* indices, int64_t B,
   return SOM_OK;
 }
 
-// Resolved knobs.  Defaults chosen by measurement on MI355X (512^2 map,
-// F = 20,000, 1M-document batches).
+// Resolved knobs.  The automatic choices follow measurements on MI355X (512^2
+// and 256^2 maps, F = 20,000, 1M-document batches).
 struct Plan {
   int kernel = 1;
   // kernel 1
@@ -81,19 +81,33 @@ struct Plan {
   int64_t nchunks = 0;  // neuron slices
 };
 
-som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
-                     int weights = som::kWeightsF32) {
+// Kernel-1 tiles per workgroup chosen automatically: four consecutive tiles
+// of 16 documents share one CU (and its vector L1) on large fp32 maps, where
+// it ran a 1M-document batch of the 512^2 map 2.9% faster; one elsewhere (the
+// 256^2 map and fp16 codebooks were neutral or slower).
+constexpr int64_t kGroupTilesMinN = 131072;
+
+// `weights` is the storage type of the codebook searched (it fixes the load
+// width K); `auto_weights` the one the automatic tile size is chosen for:
+// the entry point's own type when it plans internally, opts->storage for
+// som_plan and the planned searches, so that a plan and its search always
+// resolve the same tile geometry.
+som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, int weights, int auto_weights) {
   som_bmu_opts o{};
   if (opts) o = *opts;
   const bool f16 = weights == som::kWeightsF16;
+  const bool auto16 = auto_weights == som::kWeightsF16;
   if (f16 && o.kernel == 2) return fail(SOM_ERR_INVALID_ARG, "an fp16 codebook is searched by kernels 1 and 3 only");
-  if (o.reserved != 0) return fail(SOM_ERR_INVALID_ARG, "opts->reserved must be 0");
+  if (o.storage != 0 && o.storage != 1) return fail(SOM_ERR_INVALID_ARG, "opts->storage must be 0 (fp32) or 1 (fp16)");
   if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
   if (o.kernel < 0 || o.kernel > 3) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1, 2 or 3");
   const int kernel = o.kernel ? o.kernel : 1;
   p->kernel = kernel;
   if (kernel == 1) {
-    const int T = o.tile_docs ? o.tile_docs : 8;
+    // automatic tile size: 16 documents for fp32 (about 5% faster than 8 on
+    // the 512^2 map), 8 for fp16 (whose 512-neuron slices leave fewer
+    // registers for accumulators)
+    const int T = o.tile_docs ? o.tile_docs : (auto16 ? 8 : 16);
     if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16 && T != 32)
       return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 1, 2, 4, 8, 16 or 32");
     if (f16 && T == 32) return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs 32 is not available for an fp16 codebook");
@@ -101,7 +115,7 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
     if (K != 4 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0, 4 or 8");
     if (T == 32 && K != 4) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 4 when tile_docs is 32");
     if (f16 && K != 8) return fail(SOM_ERR_INVALID_ARG, "opts->lane_neurons must be 0 or 8 for an fp16 codebook");
-    const int G = o.group_tiles ? o.group_tiles : 1;
+    const int G = o.group_tiles ? o.group_tiles : ((!f16 && !auto16 && T == 16 && N >= kGroupTilesMinN) ? 4 : 1);
     if (G != 1 && G != 2 && G != 4 && G != 8)
       return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles must be 0, 1, 2, 4 or 8 for kernel 1");
     if (o.mask_mode < 0 || o.mask_mode > 2) return fail(SOM_ERR_INVALID_ARG, "opts->mask_mode must be 0, 1 or 2");
@@ -149,6 +163,11 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p,
   if (p->nchunks > 65535)
     return fail(SOM_ERR_INVALID_ARG, "too many neuron slices for one launch (N / slice width must be <= 65535)");
   return SOM_OK;
+}
+
+// Storage type named by the options (for som_plan and the planned searches).
+int opts_storage(const som_bmu_opts* opts) {
+  return (opts && opts->storage == 1) ? som::kWeightsF16 : som::kWeightsF32;
 }
 
 size_t take(size_t& o, size_t bytes) {
@@ -288,7 +307,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 11; }
+int32_t som_abi_version(void) { return 12; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -319,11 +338,25 @@ som_status som_codebook_norms_f16(const uint16_t* W, int64_t F, int64_t N, int64
   return norms_impl(W, som::kWeightsF16, F, N, ldw, norms, stream);
 }
 
+// Workspace of a search that plans internally: the automatic tile size
+// depends on the storage type of the entry point called, so the size covers
+// both (an fp16 tile plan has more, smaller tiles).
+static size_t search_ws_bytes(int64_t N, int64_t B, int64_t nnz, const som_bmu_opts* opts) {
+  size_t need = 0;
+  for (int w : {som::kWeightsF32, som::kWeightsF16}) {
+    Plan p;
+    if (make_plan(N, B, opts, &p, w, w) != SOM_OK) continue;
+    const size_t t = search_ws(p, B, nnz, opts && opts->validate).total;
+    need = t > need ? t : need;
+  }
+  return need;
+}
+
 size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz, const som_bmu_opts* opts) {
   if (F < 1 || N < 1 || B < 0 || nnz < 0) return 0;
   Plan p;
-  if (make_plan(N, B, opts, &p) != SOM_OK) return 0;
-  return search_ws(p, B, nnz, opts && opts->validate).total;
+  if (make_plan(N, B, opts, &p, som::kWeightsF32, som::kWeightsF32) != SOM_OK) return 0;
+  return search_ws_bytes(N, B, nnz, opts);
 }
 
 static som_status search_impl(const void* W, int weights, int64_t F, int64_t N, int64_t ldw,
@@ -339,7 +372,7 @@ static som_status search_impl(const void* W, int weights, int64_t F, int64_t N, 
   if (B > 0 && (!bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "bmu or dist is NULL");
   if (top2 && B > 0 && (!bmu2 || !dist2)) return fail(SOM_ERR_INVALID_ARG, "bmu2 or dist2 is NULL");
   Plan p;
-  s = make_plan(N, B, opts, &p, weights);
+  s = make_plan(N, B, opts, &p, weights, weights);
   if (s != SOM_OK) return s;
   const bool validate = opts && opts->validate;
   const SearchWs w = search_ws(p, B, nnz, validate);
@@ -396,7 +429,8 @@ som_status som_bmu_search_top2_f16(const uint16_t* W, int64_t F, int64_t N, int6
 size_t som_plan_bytes(int64_t B, int64_t nnz, const som_bmu_opts* opts) {
   if (B < 0 || nnz < 0) return 0;
   Plan p;
-  if (make_plan(1, B, opts, &p) != SOM_OK) return 0;
+  const int st = opts_storage(opts);
+  if (make_plan(1, B, opts, &p, st, st) != SOM_OK) return 0;
   return plan_layout(p, nnz).total;
 }
 
@@ -408,7 +442,8 @@ som_status som_plan(const int32_t* indptr, const int32_t* indices, int64_t B, in
   if (F < 1 || F > kI32Max) return fail(SOM_ERR_INVALID_ARG, "F must be in [1, 2^31)");
   if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate applies to som_bmu_search only");
   Plan p;
-  s = make_plan(1, B, opts, &p);
+  const int st = opts_storage(opts);
+  s = make_plan(1, B, opts, &p, st, st);
   if (s != SOM_OK) return s;
   const PlanLayout l = plan_layout(p, nnz);
   if (B == 0) return ok();
@@ -424,7 +459,7 @@ som_status som_plan(const int32_t* indptr, const int32_t* indices, int64_t B, in
 size_t som_bmu_search_planned_workspace_bytes(int64_t N, int64_t B, const som_bmu_opts* opts) {
   if (N < 1 || B < 0) return 0;
   Plan p;
-  if (make_plan(N, B, opts, &p) != SOM_OK) return 0;
+  if (make_plan(N, B, opts, &p, opts_storage(opts), opts_storage(opts)) != SOM_OK) return 0;
   return keys_bytes(B);
 }
 
@@ -440,7 +475,7 @@ static som_status planned_impl(const void* W, int weights, int64_t F, int64_t N,
   if (nnz < 0 || nnz > kI32Max) return fail(SOM_ERR_INVALID_ARG, "nnz must be in [0, 2^31)");
   if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on a planned search");
   Plan p;
-  s = make_plan(N, B, opts, &p, weights);
+  s = make_plan(N, B, opts, &p, weights, opts_storage(opts));
   if (s != SOM_OK) return s;
   const PlanLayout l = plan_layout(p, nnz);
   if (B == 0) return ok();
@@ -541,12 +576,11 @@ som_status som_group_plan(const int32_t* indptr, const int32_t* indices, int64_t
 
 size_t som_cluster_workspace_bytes(int64_t B, int64_t F, int64_t nnz) {
   if (B < 0 || F < 1 || nnz < 0 || B >= kI32Max) return 0;
+  const int64_t n2 = som::cluster_sort_size(B);
   size_t o = 0;
-  take(o, sizeof(int32_t) * F);   // df
-  take(o, sizeof(uint64_t) * B);  // keys
-  take(o, sizeof(uint64_t) * B);  // sorted keys
-  take(o, sizeof(int32_t) * B);   // iota
-  take(o, som::cluster_sort_temp_bytes(B, F));
+  take(o, sizeof(int32_t) * F);    // df
+  take(o, sizeof(uint64_t) * n2);  // signature keys (padded to a power of two)
+  take(o, sizeof(uint32_t) * n2);  // input positions
   return o;
 }
 
@@ -563,16 +597,13 @@ som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int6
   const size_t need = som_cluster_workspace_bytes(B, F, nnz);
   if (ws_bytes < need)
     return fail(SOM_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
+  const int64_t n2 = som::cluster_sort_size(B);
   size_t o = 0;
   const size_t o_df = take(o, sizeof(int32_t) * F);
-  const size_t o_keys = take(o, sizeof(uint64_t) * B);
-  const size_t o_sorted = take(o, sizeof(uint64_t) * B);
-  const size_t o_iota = take(o, sizeof(int32_t) * B);
-  const size_t tb = som::cluster_sort_temp_bytes(B, F);
-  const size_t o_tmp = take(o, tb);
+  const size_t o_keys = take(o, sizeof(uint64_t) * n2);
+  const size_t o_vals = take(o, sizeof(uint32_t) * n2);
   hipError_t e = som::launch_cluster(indptr, indices, B, F, nnz, perm, at<int32_t>(ws, o_df),
-                                     at<uint64_t>(ws, o_keys), at<uint64_t>(ws, o_sorted),
-                                     at<int32_t>(ws, o_iota), at<void>(ws, o_tmp), tb, stream);
+                                     at<uint64_t>(ws, o_keys), at<uint32_t>(ws, o_vals), stream);
   if (e != hipSuccess) return hip_fail(e, "cluster launch");
   return ok();
 }
@@ -596,7 +627,7 @@ static UnfusedWs unfused_ws(const Plan& p, int64_t N, int64_t nnz, int64_t block
 }
 
 static som_status unfused_plan(int64_t N, int64_t B, const som_bmu_opts* opts, int64_t block_docs, Plan* p) {
-  som_status s = make_plan(N, B, opts, p);
+  som_status s = make_plan(N, B, opts, p, som::kWeightsF32, som::kWeightsF32);
   if (s != SOM_OK) return s;
   if (p->kernel != 1) return fail(SOM_ERR_INVALID_ARG, "the unfused comparator uses kernel 1");
   if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on the unfused comparator");

@@ -4,12 +4,12 @@
 //   df(f)  = number of documents of the batch containing f
 //   (s1,s2)= a document's two features of highest df (ties to the lower id;
 //            F stands in for a missing feature)
-//   order  = stable sort of the documents by (s1, s2), i.e. by
-//            (s1, s2, input position).
-// Integer work; deterministic.  The stable key sort is a library radix
-// sort (hipCUB); the histogram and signatures are our kernels.
-#include <hipcub/hipcub.hpp>
-
+//   order  = the documents sorted by (s1, s2, input position).
+// Integer work; deterministic.  Every kernel here is the library's own: an
+// LDS-windowed df histogram, one signature per document, and a bitonic
+// sorting network over (signature, input position) pairs.  Since the input
+// position makes every pair distinct, the network's (unstable) sort yields
+// exactly the stable order by signature.
 #include "common.h"
 
 namespace som {
@@ -39,17 +39,19 @@ __global__ void k_zero_i32(int32_t* __restrict__ p, int64_t n) {
   if (i < n) p[i] = 0;
 }
 
-__global__ void k_iota(int32_t* __restrict__ p, int64_t n) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = static_cast<int32_t>(i);
-}
-
-// Signature key of each document: (s1 << bits) | s2.
+// Signature key of each document at position d < B: key (s1 << bits) | s2,
+// value d; positions B .. n2-1 are padding that sorts after every document.
 __global__ void __launch_bounds__(256)
-k_signature(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, int64_t B,
-            int64_t F, int bits, const int32_t* __restrict__ df, uint64_t* __restrict__ keys) {
+k_signature(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, int64_t B, int64_t n2,
+            int64_t F, int bits, const int32_t* __restrict__ df, uint64_t* __restrict__ keys,
+            uint32_t* __restrict__ vals) {
   const int64_t d = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (d >= B) return;
+  if (d >= n2) return;
+  if (d >= B) {
+    keys[d] = ~0ull;
+    vals[d] = 0xffffffffu;
+    return;
+  }
   int64_t s1 = F, s2 = F;
   int32_t c1 = -1, c2 = -1;  // df of s1, s2
   for (int32_t i = indptr[d]; i < indptr[d + 1]; ++i) {
@@ -64,6 +66,7 @@ k_signature(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indi
     }
   }
   keys[d] = (static_cast<uint64_t>(s1) << bits) | static_cast<uint64_t>(s2);
+  vals[d] = static_cast<uint32_t>(d);
 }
 
 int key_bits(int64_t F) {
@@ -72,21 +75,96 @@ int key_bits(int64_t F) {
   return b;
 }
 
+// ---------------------------------------------------------------------------
+// Bitonic sort of n2 (a power of two) pairs (key, val), ascending in the
+// pair order.  Step (k, j) compares element i with i ^ j for every i whose
+// bit j is clear, in ascending direction when bit k of i is clear and
+// descending otherwise; k runs over 2, 4, .., n2 and, for each k, j over
+// k/2, k/4, .., 1.  Steps with j < kLocal stay inside aligned blocks of
+// kLocal elements and run in LDS (one launch for a run of them); wider
+// steps run one launch each over global memory.
+// ---------------------------------------------------------------------------
+constexpr int kLocal = 2048;           // elements per LDS block
+constexpr int kLocalThreads = kLocal / 2;
+
+__device__ __forceinline__ bool pair_greater(uint64_t ka, uint32_t va, uint64_t kb, uint32_t vb) {
+  return ka > kb || (ka == kb && va > vb);
+}
+
+// Steps (k, j) for k = k_lo .. k_hi and, for each k, j from (k == k_lo ?
+// j_first : k/2) down to 1, on blocks of `blk` elements (blk = min(kLocal,
+// n2), blk / 2 threads per block, one compared pair per thread and step).
+__global__ void __launch_bounds__(kLocalThreads)
+k_bitonic_local(uint64_t* __restrict__ keys, uint32_t* __restrict__ vals, int64_t blk, int64_t k_lo, int64_t k_hi,
+                int64_t j_first) {
+  __shared__ uint64_t sk[kLocal];
+  __shared__ uint32_t sv[kLocal];
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * blk;
+  const int t = threadIdx.x;
+  for (int64_t i = t; i < blk; i += blockDim.x) {
+    sk[i] = keys[base + i];
+    sv[i] = vals[base + i];
+  }
+  __syncthreads();
+  for (int64_t k = k_lo; k <= k_hi; k <<= 1) {
+    for (int64_t j = (k == k_lo ? j_first : k >> 1); j > 0; j >>= 1) {
+      // thread t's pair: insert a clear bit j into t (j is a power of two)
+      const int64_t i = ((t & ~(j - 1)) << 1) | (t & (j - 1));
+      const int64_t l = i + j;
+      const bool asc = ((base + i) & k) == 0;
+      const uint64_t ka = sk[i], kb = sk[l];
+      const uint32_t va = sv[i], vb = sv[l];
+      if (pair_greater(ka, va, kb, vb) == asc) {
+        sk[i] = kb;
+        sv[i] = vb;
+        sk[l] = ka;
+        sv[l] = va;
+      }
+      __syncthreads();
+    }
+  }
+  for (int64_t i = t; i < blk; i += blockDim.x) {
+    keys[base + i] = sk[i];
+    vals[base + i] = sv[i];
+  }
+}
+
+// One step (k, j) with j >= kLocal over all n2 elements: thread t compares
+// the pair (i, i + j), i being t with a clear bit j inserted.
+__global__ void __launch_bounds__(256)
+k_bitonic_global(uint64_t* __restrict__ keys, uint32_t* __restrict__ vals, int64_t n2, int64_t k, int64_t j) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= n2 / 2) return;
+  const int64_t i = ((t & ~(j - 1)) << 1) | (t & (j - 1));
+  const int64_t l = i + j;
+  const bool asc = (i & k) == 0;
+  const uint64_t ka = keys[i], kb = keys[l];
+  const uint32_t va = vals[i], vb = vals[l];
+  if (pair_greater(ka, va, kb, vb) == asc) {
+    keys[i] = kb;
+    vals[i] = vb;
+    keys[l] = ka;
+    vals[l] = va;
+  }
+}
+
+__global__ void __launch_bounds__(256)
+k_perm_out(const uint32_t* __restrict__ vals, int64_t B, int32_t* __restrict__ perm) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < B) perm[i] = static_cast<int32_t>(vals[i]);
+}
+
 }  // namespace
 
-size_t cluster_sort_temp_bytes(int64_t B, int64_t F) {
-  size_t bytes = 0;
-  const hipError_t e = hipcub::DeviceRadixSort::SortPairs(nullptr, bytes, static_cast<const uint64_t*>(nullptr),
-                                     static_cast<uint64_t*>(nullptr), static_cast<const int32_t*>(nullptr),
-                                     static_cast<int32_t*>(nullptr), static_cast<int>(B), 0,
-                                     2 * key_bits(F));
-  return e == hipSuccess ? bytes : 0;
+int64_t cluster_sort_size(int64_t B) {
+  int64_t n2 = 1;
+  while (n2 < B) n2 <<= 1;
+  return n2;
 }
 
 hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
-                          int64_t nnz, int32_t* perm, int32_t* df, uint64_t* keys,
-                          uint64_t* keys_sorted, int32_t* iota, void* sort_temp,
-                          size_t sort_temp_bytes, hipStream_t stream) {
+                          int64_t nnz, int32_t* perm, int32_t* df, uint64_t* keys, uint32_t* vals,
+                          hipStream_t stream) {
   hipLaunchKernelGGL(k_zero_i32, dim3(static_cast<uint32_t>((F + 255) / 256)), dim3(256), 0, stream, df, F);
   if (nnz > 0) {
     const uint32_t groups = static_cast<uint32_t>((nnz + kHistItems - 1) / kHistItems);
@@ -96,14 +174,25 @@ hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t
     }
   }
   const int bits = key_bits(F);
-  hipLaunchKernelGGL(k_signature, dim3(static_cast<uint32_t>((B + 255) / 256)), dim3(256), 0, stream,
-                     indptr, indices, B, F, bits, df, keys);
-  hipLaunchKernelGGL(k_iota, dim3(static_cast<uint32_t>((B + 255) / 256)), dim3(256), 0, stream, iota, B);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  size_t tb = sort_temp_bytes;
-  return hipcub::DeviceRadixSort::SortPairs(sort_temp, tb, keys, keys_sorted, iota, perm,
-                                            static_cast<int>(B), 0, 2 * bits, stream);
+  const int64_t n2 = cluster_sort_size(B);
+  hipLaunchKernelGGL(k_signature, dim3(static_cast<uint32_t>((n2 + 255) / 256)), dim3(256), 0, stream,
+                     indptr, indices, B, n2, F, bits, df, keys, vals);
+  if (n2 >= 2) {
+    const int64_t blk = n2 < kLocal ? n2 : kLocal;
+    const uint32_t nblk = static_cast<uint32_t>(n2 / blk);
+    // every step with k <= blk inside the blocks
+    hipLaunchKernelGGL(k_bitonic_local, dim3(nblk), dim3(static_cast<uint32_t>(blk / 2)), 0, stream, keys, vals,
+                       blk, int64_t(2), blk, int64_t(1));
+    for (int64_t k = 2 * blk; k <= n2; k <<= 1) {
+      for (int64_t j = k >> 1; j >= blk; j >>= 1)
+        hipLaunchKernelGGL(k_bitonic_global, dim3(static_cast<uint32_t>((n2 / 2 + 255) / 256)), dim3(256), 0,
+                           stream, keys, vals, n2, k, j);
+      hipLaunchKernelGGL(k_bitonic_local, dim3(nblk), dim3(static_cast<uint32_t>(blk / 2)), 0, stream, keys, vals,
+                         blk, k, k, blk >> 1);
+    }
+  }
+  hipLaunchKernelGGL(k_perm_out, dim3(static_cast<uint32_t>((B + 255) / 256)), dim3(256), 0, stream, vals, B, perm);
+  return hipGetLastError();
 }
 
 }  // namespace som

@@ -125,11 +125,11 @@ hipError_t launch_update_finish(void* W, int weights, int64_t F, int64_t ldw, in
 // Read-bandwidth probe (probe.hip): `passes` grid-stride reads of buf.
 hipError_t launch_read_probe(const void* buf, int64_t bytes, int32_t passes, uint32_t* sink, hipStream_t stream);
 
-// Clustering.
-size_t cluster_sort_temp_bytes(int64_t B, int64_t F);
+// Clustering: df histogram, signatures and a bitonic sort of n2 =
+// cluster_sort_size(B) (a power of two >= B) (key, position) pairs.
+int64_t cluster_sort_size(int64_t B);
 hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
-                          int64_t nnz, int32_t* perm, int32_t* df, uint64_t* keys,
-                          uint64_t* keys_sorted, int32_t* iota, void* sort_temp,
-                          size_t sort_temp_bytes, hipStream_t stream);
+                          int64_t nnz, int32_t* perm, int32_t* df, uint64_t* keys, uint32_t* vals,
+                          hipStream_t stream);
 
 }  // namespace som

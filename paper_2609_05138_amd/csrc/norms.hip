@@ -48,7 +48,9 @@ k_norms(const WT* __restrict__ W, int64_t F, int64_t N, int64_t ldw, float* __re
   const int wave = threadIdx.x >> 6;
   const int64_t col = (static_cast<int64_t>(blockIdx.x) * 64 + lane) * E;  // first of E neurons
   double s[kChains][E] = {};
-  if (col < ldw) {
+  // only groups holding a neuron j < N are read: no load leaves
+  // [0, round_up(N, E)) of its row
+  if (col < N) {
     const WT* base = W + col;
     int64_t f = wave;
     // rows f, f + 8, f + 16, f + 24 go to chains 0..3, in increasing f per chain
@@ -92,11 +94,11 @@ k_norms(const WT* __restrict__ W, int64_t F, int64_t N, int64_t ldw, float* __re
 hipError_t launch_norms(const void* W, int weights, int64_t F, int64_t N, int64_t ldw, float* norms,
                         hipStream_t stream) {
   if (weights == kWeightsF16) {
-    const int64_t groups = (ldw / 8 + 63) / 64;
+    const int64_t groups = ((N + 7) / 8 + 63) / 64;
     hipLaunchKernelGGL(k_norms<_Float16>, dim3(static_cast<uint32_t>(groups)), dim3(kNormWaves * 64), 0, stream,
                        static_cast<const _Float16*>(W), F, N, ldw, norms);
   } else {
-    const int64_t groups = (ldw / 4 + 63) / 64;
+    const int64_t groups = ((N + 3) / 4 + 63) / 64;
     hipLaunchKernelGGL(k_norms<float>, dim3(static_cast<uint32_t>(groups)), dim3(kNormWaves * 64), 0, stream,
                        static_cast<const float*>(W), F, N, ldw, norms);
   }

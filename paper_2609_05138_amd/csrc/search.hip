@@ -56,10 +56,12 @@ k_search_docs(SearchArgs a) {
   const int64_t ldw = a.ldw;
 
   // staging role: row r = pass * kRpp + tid / kTpr, float4 q = tid % kTpr;
-  // columns past the row end re-read the row's last float4 (in bounds)
+  // columns past the last neuron re-read the last float4 holding one, so no
+  // load leaves [0, round_up(N, 4)) of its row
   const int sq = tid % kTpr;
   const int sr = tid / kTpr;
-  const int64_t scol = n0 + 4 * sq < ldw ? n0 + 4 * sq : ldw - 4;
+  const int64_t nv = (a.N + 3) / 4 * 4;
+  const int64_t scol = n0 + 4 * sq < nv ? n0 + 4 * sq : nv - 4;
   const float* __restrict__ Wc = static_cast<const float*>(a.W) + scol;
   float4 stage[kPasses];
 #pragma unroll

@@ -312,12 +312,14 @@ k_search(SearchArgs a) {
 
   // Load q of a lane covers neurons n0 + 64*E*q + E*lane + [0, E), which are
   // accumulators E*q .. E*q + E - 1.  Byte offsets inside a row slice; lanes
-  // past the row end re-read the row's last group (in bounds, never reported).
+  // past the last neuron re-read the last group holding one (never reported),
+  // so no load leaves [0, round_up(N, E)) of its row.
+  const int64_t nv = (a.N + E - 1) / E * E;
   uint32_t offb[Q];
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int64_t o = 64 * E * q + E * lane;
-    offb[q] = static_cast<uint32_t>(sizeof(WT) * (n0 + o < a.ldw ? o : a.ldw - E - n0));
+    offb[q] = static_cast<uint32_t>(sizeof(WT) * (n0 + o < nv ? o : nv - E - n0));
   }
   const int32_t u0 = a.tile_offset[t];
   const int32_t cnt = a.tile_count[t];

@@ -109,9 +109,11 @@ k_search_st(SearchArgs a) {
 #pragma unroll
     for (int k = 0; k < K; ++k) acc[s][k] = 0.f;
 
-  // lanes past the row end re-read the row's last 128-bit group (in bounds)
+  // lanes past the last neuron re-read the last 128-bit group holding one, so
+  // no load leaves [0, round_up(N, E)) of its row
   const int64_t o = E * lane;
-  const uint32_t offb = static_cast<uint32_t>(sizeof(WT) * (n0 + o < a.ldw ? o : a.ldw - E - n0));
+  const int64_t nv = (a.N + E - 1) / E * E;
+  const uint32_t offb = static_cast<uint32_t>(sizeof(WT) * (n0 + o < nv ? o : nv - E - n0));
   const char* __restrict__ Wn = reinterpret_cast<const char*>(static_cast<const WT*>(a.W) + n0) + offb;
   const int64_t ldw_b = a.ldw * static_cast<int64_t>(sizeof(WT));
   const int32_t u0 = a.tile_offset[st];

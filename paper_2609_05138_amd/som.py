@@ -69,7 +69,7 @@ class som_bmu_opts(ctypes.Structure):
         ("mask_mode", ctypes.c_int32),
         ("slice_neurons", ctypes.c_int32),
         ("validate", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("storage", ctypes.c_int32),
     ]
 
 
@@ -187,9 +187,20 @@ def _stream(stream) -> ctypes.c_void_p:
 
 
 def _opts(kernel=0, tile_docs=0, lane_neurons=0, group_tiles=0, mask_mode=0, slice_neurons=0,
-          validate=False) -> som_bmu_opts:
+          validate=False, storage=0) -> som_bmu_opts:
     return som_bmu_opts(int(kernel), int(tile_docs), int(lane_neurons), int(group_tiles), int(mask_mode),
-                        int(slice_neurons), int(bool(validate)), 0)
+                        int(slice_neurons), int(bool(validate)), int(storage))
+
+
+def _n_neurons(N, norms, W) -> int:
+    """N of a search: explicit, else the length of the norms vector.
+
+    The codebook's second dimension is its row stride, which may exceed N
+    (padding to the recommended stride); its padding columns are not
+    neurons, so they are never the default."""
+    if N is not None:
+        return int(N)
+    return int(norms.numel())
 
 
 def _workspace(nbytes: int, device) -> torch.Tensor:
@@ -212,11 +223,14 @@ def som_codebook_ldw(N: int) -> int:
 
 def som_codebook_norms(W: torch.Tensor, N: Optional[int] = None, norms: Optional[torch.Tensor] = None,
                        stream=None) -> torch.Tensor:
-    """||w_j||^2 for j < N of the feature-major codebook W [F, ldw] (fp32 or fp16)."""
+    """||w_j||^2 for j < N of the feature-major codebook W [F, ldw] (fp32 or fp16).
+
+    N defaults to the length of ``norms`` when it is given, else to ldw (a
+    codebook padded beyond N needs N)."""
     lib = load()
     sfx = _codebook(W)
     F, ldw = W.shape
-    n = ldw if N is None else int(N)
+    n = int(N) if N is not None else (int(norms.numel()) if norms is not None else ldw)
     if norms is None:
         norms = torch.empty(n, dtype=torch.float32, device=W.device)
     _dev(norms, torch.float32, "norms")
@@ -250,7 +264,7 @@ def _search(top2, W, norms, indptr, indices, N, perm, validate, outs, ws, stream
     _dev(indptr, torch.int32, "indptr")
     _dev(indices, torch.int32, "indices")
     F, ldw = W.shape
-    n = ldw if N is None else int(N)
+    n = _n_neurons(N, norms, W)
     if norms.numel() < n:
         raise ValueError("norms must hold at least N values")
     B = indptr.numel() - 1
@@ -281,8 +295,9 @@ def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, i
                    ws: Optional[torch.Tensor] = None, stream=None, **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
     """BMU index (int32) and squared distance (fp32) of every CSR document.
 
-    ``knobs``: kernel, tile_docs, lane_neurons, group_tiles, mask_mode,
-    slice_neurons (fields of som_bmu_opts; none changes a result)."""
+    ``N`` defaults to the length of ``norms``.  ``knobs``: kernel, tile_docs,
+    lane_neurons, group_tiles, mask_mode, slice_neurons (fields of
+    som_bmu_opts; none changes a result)."""
     return _search(False, W, norms, indptr, indices, N, perm, validate, (bmu, dist), ws, stream, knobs)
 
 
@@ -310,7 +325,12 @@ class Plan:
 
 def som_plan(indptr: torch.Tensor, indices: torch.Tensor, F: int, perm: Optional[torch.Tensor] = None,
              plan: Optional[torch.Tensor] = None, stream=None, **knobs) -> Plan:
-    """Plan of a batch for som_bmu_search_planned (codebook-independent)."""
+    """Plan of a batch for som_bmu_search_planned (codebook-independent).
+
+    ``knobs`` as for som_bmu_search, plus ``storage`` (0 = fp32, 1 = fp16):
+    the storage type whose automatic tile size the plan takes; the planned
+    search resolves the same geometry from the plan's knobs, whatever the
+    codebook it is given."""
     lib = load()
     _dev(indptr, torch.int32, "indptr")
     _dev(indices, torch.int32, "indices")
@@ -339,7 +359,7 @@ def _planned(top2, W, norms, indptr, plan, N, outs, ws, stream):
     _dev(norms, torch.float32, "norms")
     _dev(indptr, torch.int32, "indptr")
     F, ldw = W.shape
-    n = ldw if N is None else int(N)
+    n = _n_neurons(N, norms, W)
     if norms.numel() < n:
         raise ValueError("norms must hold at least N values")
     B = indptr.numel() - 1
@@ -502,7 +522,7 @@ def som_bmu_search_unfused(W: torch.Tensor, norms: torch.Tensor, indptr: torch.T
     _dev(indptr, torch.int32, "indptr")
     _dev(indices, torch.int32, "indices")
     F, ldw = W.shape
-    n = ldw if N is None else int(N)
+    n = _n_neurons(N, norms, W)
     if norms.numel() < n:
         raise ValueError("norms must hold at least N values")
     B = indptr.numel() - 1

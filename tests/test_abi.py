@@ -42,7 +42,28 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 11
+    assert som.som_abi_version() == 12
+
+
+def test_automatic_tile_size_follows_the_storage_type(lib):
+    # som_plan resolves the automatic tile size from opts->storage: 16
+    # documents for fp32, 8 for fp16 (twice the tiles, so larger per-tile
+    # arrays); explicit sizes do not depend on it
+    B, nnz = 1 << 20, 84_000_000
+    f32, f16 = som.som_bmu_opts(), som.som_bmu_opts()
+    f16.storage = 1
+    p32 = lib.som_plan_bytes(B, nnz, ctypes.byref(f32))
+    p16 = lib.som_plan_bytes(B, nnz, ctypes.byref(f16))
+    assert p16 - p32 >= 8 * (B // 8 - B // 16)
+    t8, t8h = som.som_bmu_opts(1, 8), som.som_bmu_opts(1, 8)
+    t8h.storage = 1
+    assert lib.som_plan_bytes(B, nnz, ctypes.byref(t8)) == lib.som_plan_bytes(B, nnz, ctypes.byref(t8h)) == p16
+    # a search that plans internally may be either storage type: its
+    # workspace covers the larger (fp16) automatic plan
+    assert lib.som_bmu_workspace_bytes(20000, 262144, B, nnz, None) >= p16 + 8 * B
+    # the planned workspace holds keys only
+    assert (lib.som_bmu_search_planned_workspace_bytes(262144, B, ctypes.byref(f16))
+            == lib.som_bmu_search_planned_workspace_bytes(262144, B, ctypes.byref(f32)))
 
 
 def test_probe_rejects_bad_arguments(lib):
@@ -136,7 +157,7 @@ def test_search_rejects_bad_arguments(lib):
     assert call(ws=null)[0] == som.SOM_ERR_WORKSPACE
     assert call(ws=ws_bad)[0] == som.SOM_ERR_INVALID_ARG
     res = som.som_bmu_opts()
-    res.reserved = 1
+    res.storage = 2
     O = som.som_bmu_opts
     for bad in (O(4), O(-1), O(3, 32), O(3, 16), O(3, 0, 8), O(3, 0, 0, 2), O(3, 0, 0, 0, 1), O(3, 0, 0, 0, 0, 32),
                 O(1, 5), O(1, 0, 3), res, O(1, 0, 0, 16), O(1, 0, 0, 0, 3), O(1, 32, 8),
