@@ -163,6 +163,27 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
                           const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* som_bmu_search without a workspace argument and without any allocation,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The
+ * workspace comes from a static device array of SOM_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) that each GPU the library runs on holds until the process ends;
+ * the call itself allocates nothing and needs
+ * som_bmu_workspace_bytes(F, N, B, nnz, opts) <= SOM_NOALLOC_SCRATCH_BYTES
+ * (e.g. batches of 65,536 documents of 80 features), else it returns
+ * SOM_ERR_INVALID_ARG before any HIP call.  Its first call on a device
+ * looks up the array's address there (with that device current).
+ * Arguments, results and errors as for som_bmu_search with an fp32
+ * codebook; opts->validate must be 0 (validation synchronises).  Every call
+ * on one GPU uses that GPU's one array: calls whose work overlaps on a GPU
+ * (different streams, or threads) race and must be serialised by the
+ * caller; calls in one stream order are safe. */
+#define SOM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+som_status som_bmu_search_noalloc(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                                  const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                  const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                                  hipStream_t stream);
+
 /* Best AND second-best unit of each document in the same fused pass (the
  * paper's kernel keeps the second-best unit because the topographic error,
  * on which both of its stopping rules depend, needs it: Section 6.2, Table 5;

@@ -3,6 +3,7 @@
 // memory; every array comes from the caller.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 #include <string>
 
 #include "../../include/som.h"
@@ -397,6 +398,80 @@ som_status som_bmu_search(const float* W, int64_t F, int64_t N, int64_t ldw, con
                           void* ws, size_t ws_bytes, hipStream_t stream) {
   return search_impl(W, som::kWeightsF32, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, nullptr,
                      nullptr, false, opts, ws, ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free search: the workspace of som_bmu_search (plan and packed
+// keys) lives in a file-scope device array instead of a caller's buffer.
+// ---------------------------------------------------------------------------
+
+}  // extern "C"
+
+// One copy per GPU, held from the library's load until the process ends.  In
+// host code `scratch` names a host-side stand-in: its device address is
+// looked up (hipGetSymbolAddress) once per device and only that address is
+// ever passed to kernels.
+static __device__ __align__(256) unsigned char scratch[SOM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on that device, with the device current).
+som_status noalloc_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(SOM_ERR_INVALID_ARG, "current device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(SOM_ERR_HIP, "hipGetSymbolAddress(scratch) returned no address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SOM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+som_status som_bmu_search_noalloc(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,
+                                  const int32_t* indptr, const int32_t* indices, int64_t B, int64_t nnz,
+                                  const int32_t* perm, int32_t* bmu, float* dist, const som_bmu_opts* opts,
+                                  hipStream_t stream) {
+  // every check and the size limit come before any HIP call
+  som_status s = check_codebook(W, som::kWeightsF32, F, N, ldw);
+  if (s != SOM_OK) return s;
+  if (!norms) return fail(SOM_ERR_INVALID_ARG, "norms is NULL");
+  s = check_batch(indptr, indices, B, nnz);
+  if (s != SOM_OK) return s;
+  if (B > 0 && (!bmu || !dist)) return fail(SOM_ERR_INVALID_ARG, "bmu or dist is NULL");
+  if (opts && opts->validate)
+    return fail(SOM_ERR_INVALID_ARG, "validate synchronises the stream: not available on the allocation-free search");
+  Plan p;
+  s = make_plan(N, B, opts, &p, som::kWeightsF32, som::kWeightsF32);
+  if (s != SOM_OK) return s;
+  const size_t need = search_ws(p, B, nnz, false).total;
+  if (need > SOM_NOALLOC_SCRATCH_BYTES)
+    return fail(SOM_ERR_INVALID_ARG, "this batch needs " + std::to_string(need) +
+                                         " bytes of workspace, more than the " +
+                                         std::to_string(SOM_NOALLOC_SCRATCH_BYTES) +
+                                         " the allocation-free search holds: split the batch or use som_bmu_search");
+  if (B == 0) return ok();
+  void* ws = nullptr;
+  s = noalloc_scratch(&ws);
+  if (s != SOM_OK) return s;
+  // the plan and keys are rewritten in full by each call (the keys by their
+  // own initialisation kernel), so nothing left by an earlier call is read
+  return search_impl(W, som::kWeightsF32, F, N, ldw, norms, indptr, indices, B, nnz, perm, bmu, dist, nullptr,
+                     nullptr, false, opts, ws, SOM_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 som_status som_bmu_search_top2(const float* W, int64_t F, int64_t N, int64_t ldw, const float* norms,

@@ -30,6 +30,7 @@ EXPORTS = (
     "som_bmu_workspace_bytes",
     "som_bmu_search",
     "som_bmu_search_top2",
+    "som_bmu_search_noalloc",
     "som_plan_bytes",
     "som_plan",
     "som_bmu_search_planned_workspace_bytes",
@@ -104,6 +105,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.som_bmu_search.restype = _i32
     lib.som_bmu_search.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp,
                                    ctypes.POINTER(som_bmu_opts), _vp, _sz, _vp]
+    lib.som_bmu_search_noalloc.restype = _i32
+    lib.som_bmu_search_noalloc.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp,
+                                           ctypes.POINTER(som_bmu_opts), _vp]
     lib.som_plan_bytes.restype = _sz
     lib.som_plan_bytes.argtypes = [_i64, _i64, ctypes.POINTER(som_bmu_opts)]
     lib.som_plan.restype = _i32
@@ -310,6 +314,38 @@ def som_bmu_search_top2(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tens
     (bmu2 = -1 and dist2 = +inf when N == 1)."""
     return _search(True, W, norms, indptr, indices, N, perm, validate, (bmu, dist, bmu2, dist2), ws, stream,
                    knobs)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def som_bmu_search_noalloc(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, indices: torch.Tensor,
+                           N: Optional[int] = None, perm: Optional[torch.Tensor] = None,
+                           bmu: Optional[torch.Tensor] = None, dist: Optional[torch.Tensor] = None, stream=None,
+                           **knobs) -> Tuple[torch.Tensor, torch.Tensor]:
+    """som_bmu_search whose workspace is the library's static device array
+    (no allocation by the library; fp32 codebook; bmu and dist are allocated
+    here only when not given)."""
+    lib = load()
+    _dev(W, torch.float32, "W")
+    _dev(norms, torch.float32, "norms")
+    _dev(indptr, torch.int32, "indptr")
+    _dev(indices, torch.int32, "indices")
+    F, ldw = W.shape
+    n = _n_neurons(N, norms, W)
+    if norms.numel() < n:
+        raise ValueError("norms must hold at least N values")
+    B = indptr.numel() - 1
+    if perm is not None:
+        _dev(perm, torch.int32, "perm")
+        if perm.numel() != B:
+            raise ValueError("perm must have B entries")
+    bmu, dist = _outputs(B, W.device, [(bmu, torch.int32, "bmu"), (dist, torch.float32, "dist")])
+    o = _opts(**knobs)
+    _check(lib.som_bmu_search_noalloc(_ptr(W), F, n, ldw, _ptr(norms), _ptr(indptr), _ptr(indices), B,
+                                      indices.numel(), _ptr(perm), _ptr(bmu), _ptr(dist), ctypes.byref(o),
+                                      _stream(stream)))
+    return bmu, dist
 
 
 class Plan:
