@@ -6,6 +6,8 @@ import os
 import subprocess
 import sys
 
+import numpy as np
+
 from conftest import ROOT
 
 BENCH = os.path.join(ROOT, "bench.py")
@@ -38,21 +40,47 @@ def test_help_lists_the_contract_flags():
         assert flag in r.stdout
 
 
-def test_default_launches_match_their_counter_entries():
-    # the fabric-traffic figure is reported only when the timed launch is the
-    # one the counters were taken on; a change of launch knobs must come with
-    # new counters, not with a silently missing figure
+def test_default_launch_leaves_the_knobs_to_the_library():
+    # the measured launch lives in the library (automatic tile size and tiles
+    # per workgroup); the benchmark asks only for kernel 3 where the data, which
+    # the library cannot see, favours it (128^2 map, topic workload)
+    sys.path.insert(0, ROOT)
+    import bench
+    from synth import CONFIGS
+    for argv, cfg_key, kernel, storage in ((["--config", "4"], 4, 0, 0), (["--weights", "f16"], 4, 0, 1),
+                                           (["--config", "3"], 3, 0, 0), (["--config", "5"], 5, 3, 0),
+                                           (["--config", "2"], 2, 3, 0), (["--config", "5", "--weights", "f16"], 5, 0, 1)):
+        knobs = bench.launch_knobs(bench.parse(argv), CONFIGS[cfg_key])
+        assert knobs.pop("kernel") == kernel and knobs.pop("storage") == storage, argv
+        assert not any(knobs.values()), (argv, knobs)
+
+
+def test_counter_entries_belong_to_the_current_kernels():
+    # fabric traffic is reported only from counters taken on the current kernel
+    # sources: any edit to them must come with new counters
+    sys.path.insert(0, ROOT)
+    import bench
+    digest = bench.csrc_digest()
+    for key, entry in bench.MEASURED_TRAFFIC.items():
+        assert entry["csrc"] == digest, (key, "kernel sources changed since these counters were taken")
+        assert len(entry["fetch_kib"]) == len(entry["write_kib"]) == len(json.loads(key)[1])
+
+
+def test_oracle_sample_plan():
     sys.path.insert(0, ROOT)
     import bench
     from synth import CONFIGS, batch_sizes
-    for argv, cfg_key, weights in ((["--config", "4"], 4, "f32"), (["--weights", "f16"], 4, "f16"),
-                                   (["--config", "5"], 5, "f32")):
-        args = bench.parse(argv)
-        kernel_arg, _, knobs = bench.launch_knobs(args)
-        cfg = CONFIGS[cfg_key]
-        keys = [k for k in bench.MEASURED_TRAFFIC if k[0] == cfg.name and k[4] == weights]
-        assert keys, argv
-        for k in keys:
-            assert k[1] == 0 and k[2] == batch_sizes(cfg)[0], argv
-            assert k[5] == (kernel_arg or 1), argv
-            assert k[6] == json.dumps(knobs, sort_keys=True), argv
+    for cfg_key in (3, 4, 5):
+        sizes = batch_sizes(CONFIGS[cfg_key])
+        batches = list(range(len(sizes)))
+        s = bench.sample_docs(sizes, cfg_key, batches, 2048)
+        assert sorted(s) == batches
+        total = sum(len(v) for v in s.values())
+        assert 0.9 * 2048 <= total <= 2048 + 2 * len(batches), (cfg_key, total)
+        for b, B in zip(batches, sizes):
+            assert s[b][0] == 0 and s[b][-1] == B - 1 and len(np.unique(s[b])) == len(s[b])
+    # every document of the 32^2 workload and of the first 128^2 batch
+    s = bench.sample_docs([10000], 1, [0], 2048)
+    assert np.array_equal(s[0], np.arange(10000))
+    s = bench.sample_docs([65536, 65536], 2, [0, 1], 2048)
+    assert len(s[0]) == 65536 and len(s[1]) == 1024

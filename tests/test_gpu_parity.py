@@ -456,10 +456,10 @@ def test_neuron_ranges_compose_to_the_full_search():
     W[:, 604] = W[:, 603]                                               # a tie at a range edge
     indptr, indices = _csr(docs)
     B = len(docs)
-    # a range at offset r0 may read each row's padding up to ldw elements from
-    # W + r0, so the buffer keeps ldw elements of slack after its last row
+    # a range at offset r0 reads no row beyond round_up(n, 4) elements from
+    # W + r0, so the buffer needs no slack after its last row
     ldw = 1024
-    buf = torch.zeros(F * ldw + ldw, dtype=torch.float32, device=DEV)
+    buf = torch.zeros(F * ldw, dtype=torch.float32, device=DEV)
     Wd = buf[:F * ldw].view(F, ldw)
     Wd[:, :N] = torch.from_numpy(W).to(DEV)
     norms = som.som_codebook_norms(Wd, N=N)
@@ -500,14 +500,17 @@ def test_binding_rejects_short_norms():
     norms = som.som_codebook_norms(Wd, N=90)
     ip, ix = _dev_i32(np.array([0, 2, 3])), _dev_i32(np.array([1, 7, 5]))
     with pytest.raises(ValueError):
-        som.som_bmu_search(Wd, norms, ip, ix)               # N defaults to ldw = 96
+        som.som_bmu_search(Wd, norms, ip, ix, N=96)         # the row stride is not N
     with pytest.raises(ValueError):
         som.som_bmu_search_top2(Wd, norms, ip, ix, N=91)
     plan = som.som_plan(ip, ix, 40)
     with pytest.raises(ValueError):
         som.som_bmu_search_planned(Wd, norms, ip, plan, N=96)
     bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=90)
+    # without N the binding takes the norms' length, never the padded stride
+    b0, d0 = som.som_bmu_search(Wd, norms, ip, ix)
     torch.cuda.synchronize()
+    assert torch.equal(b0, bmu) and torch.equal(d0, dist)
     W64 = W.astype(np.float64)
     _check_docs(W64, oracle.codebook_norms(W64, 90), np.array([0, 2, 3]), np.array([1, 7, 5]),
                 bmu.cpu().numpy(), dist.cpu().numpy(), range(2), N=90)

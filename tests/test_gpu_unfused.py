@@ -69,12 +69,13 @@ def test_unfused_equals_fused_config1_every_document():
     from synth import codebook, documents
     W = codebook(1)
     indptr, indices = documents(1, 0)
-    for block in (8, 64, 1000, 16384):
+    for block in (16, 64, 1008, 16384):          # multiples of the automatic 16-document tile
         f, u = _both(W, indptr, indices, block)
         assert np.array_equal(f[0], u[0]) and np.array_equal(f[1], u[1]), block
 
 
-@pytest.mark.parametrize("knobs,block", [(dict(), 8), (dict(), 200), (dict(tile_docs=16), 48),
+@pytest.mark.parametrize("knobs,block", [(dict(tile_docs=8), 8), (dict(tile_docs=8), 200), (dict(), 208),
+                                         (dict(tile_docs=16), 48),
                                          (dict(tile_docs=1, lane_neurons=8), 37),
                                          (dict(tile_docs=32), 4096), (dict(group_tiles=4, mask_mode=1), 512)])
 def test_unfused_equals_fused_ragged_map(knobs, block):
@@ -99,3 +100,39 @@ def test_unfused_equals_fused_on_the_512_map():
     indices2 = indices[keep]
     f, u = _both(Wsub, indptr2, indices2, 2048, ldw=som.som_codebook_ldw(cfg.N), tile_docs=16)
     assert np.array_equal(f[0], u[0]) and np.array_equal(f[1], u[1])
+
+
+@pytest.mark.parametrize("knobs,block", [(dict(), 208), (dict(tile_docs=1), 8), (dict(tile_docs=4), 4096)])
+def test_unfused_against_the_oracle_ragged_map(knobs, block):
+    # The comparator's own argmin pass (the 128-bit row walk and the ragged
+    # tail of N = 4,101 = 4 * 1,025 + 1 neurons) checked against the oracle,
+    # not against the fused search: 600 documents, block sizes that do not
+    # divide the batch.  Three documents get planted exact ties (two columns
+    # equal to the document's indicator: distance 0 at both), placed at the
+    # tail neuron 4100 and column 5, at two columns of different 256-column
+    # strides of the walk, and at two neighbours inside one 128-bit group;
+    # the lower index must win exactly as the oracle's first occurrence.
+    from synth import codebook, documents
+    N, F = 4101, 20000
+    W = codebook(2, N=N, F=F)
+    indptr, indices = documents(2, 1, n_docs=600)
+    planted = {0: (5, 4100), 1: (1030, 3000), 2: (2049, 2050)}
+    for d, cols in planted.items():
+        x = np.zeros(F, np.float32)
+        x[indices[indptr[d]:indptr[d + 1]]] = 1.0
+        for c in cols:
+            W[:, c] = x
+    _, (bmu, dist) = _both(W, indptr, indices, block, ldw=4104, **knobs)
+    norms64 = oracle.codebook_norms(W)
+    bad = []
+    for d in range(600):
+        feats = indices[indptr[d]:indptr[d + 1]].astype(np.int64)
+        ok, why = oracle.accept_bmu(W, norms64, feats, int(bmu[d]), float(dist[d]))
+        if not ok:
+            bad.append((d, why))
+    ref = oracle.bmu_search(W, indptr, indices, norms=norms64, docs=list(planted))
+    for i, (d, cols) in enumerate(planted.items()):
+        assert int(ref[0][i]) == cols[0] and ref[1][i] == 0.0      # the oracle: exact tie, lowest index
+        assert int(bmu[d]) == cols[0] and float(dist[d]) == 0.0, (d, int(bmu[d]), float(dist[d]))
+    print(f"[unfused {knobs} block {block}] {600 - len(bad)}/600 documents accepted by the oracle", flush=True)
+    assert not bad, bad[:5]
