@@ -79,8 +79,9 @@ typedef enum som_status {
  *   is fetched once per workgroup with 128-bit loads into LDS, and each wave
  *   (8 documents; 16 for D = 256 with an fp32 codebook) adds the rows its
  *   documents hold.
- *   Its plan is the tile plan with D-document tiles; a plan built with the
- *   same tile_docs serves both storage types.
+ *   Its plan is the tile plan with D-document tiles (with mask_mode 2, the
+ *   default, each 16-entry stage's masks stored document-major); a plan
+ *   built with the same tile_docs and mask_mode serves both storage types.
  * Every kernel cuts the neuron axis into slices whose minima are merged
  * (Section 4.2) and fuses the argmin (Section 3). */
 typedef struct som_bmu_opts {
@@ -92,7 +93,9 @@ typedef struct som_bmu_opts {
   int32_t group_tiles;   /* kernel 1: tiles per workgroup, 0 (auto: see above), 1, 2, 4 or 8;
                             kernel 2: waves per workgroup G, 0 (auto), 4, 8 or 16 */
   int32_t mask_mode;     /* kernel 1: 0 = auto, 1 = branch-free multiply by the membership
-                            bit, 2 = one scalar branch per document; kernel 3: 0 */
+                            bit, 2 = one scalar branch per document; kernel 3: 0 = auto (1),
+                            1 = one visit per needed row with a scalar branch tree over the
+                            wave's documents, 2 = one ballot per document over each stage */
   int32_t slice_neurons; /* kernel 2: NB = 0 (auto), 32 or 64 */
   int32_t validate;      /* 1 = check the CSR batch on the device first (synchronises `stream`) */
   int32_t storage;       /* 0 = fp32, 1 = fp16: the codebook storage type whose automatic tile
@@ -238,8 +241,8 @@ som_status som_bmu_search_top2_planned(const float* W, int64_t F, int64_t N, int
  * tile of T consecutive documents of the tiled order (perm as in
  * som_bmu_search; the last tile may be short) the sorted union of their
  * features and, per union entry, a T-bit membership mask (bit s set iff the
- * tile's s-th document contains the feature).  This is also the plan of
- * kernel 3 (tiles of its D documents).
+ * tile's s-th document contains the feature).  This is also the content of
+ * kernel 3's plan (tiles of its D documents).
  *   tile_docs   T in {1, 2, 4, 8, 16, 32, 64, 128, 256}
  *   tile_offset int32 [ntiles+1] output, ntiles = ceil(B / T): tile t's union
  *               is stored at [tile_offset[t], tile_offset[t] + tile_count[t]);
@@ -248,6 +251,9 @@ som_status som_bmu_search_top2_planned(const float* W, int64_t F, int64_t N, int
  *   union_feat  int32 [nnz] output (entries past each tile's count are unused)
  *   union_mask  uint32 [nnz * MW] output, MW = ceil(T / 32) words per entry:
  *               bit s of entry u is bit s % 32 of union_mask[u * MW + s / 32]
+ *               (kernel 3's own plan, by default, rearranges these bits per
+ *               16-entry stage and document; this entry point writes them
+ *               entry by entry)
  * Needs no workspace. */
 som_status som_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                          int64_t nnz, const int32_t* perm, int32_t tile_docs, int32_t* tile_offset,

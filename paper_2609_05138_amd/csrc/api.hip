@@ -80,6 +80,7 @@ struct Plan {
   int64_t D = 1024;     // documents per tile (kernel 1) or per group (kernel 2)
   int64_t nunits = 0;   // tiles or groups
   int64_t nchunks = 0;  // neuron slices
+  bool stage_masks = false;  // kernel 3, document-major: masks stored per stage and document
 };
 
 // Kernel-1 tiles per workgroup chosen automatically: four consecutive tiles
@@ -130,8 +131,9 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, in
   } else if (kernel == 3) {
     // super-tile of D documents; waves of 8 documents (16 for D = 256 with an
     // fp32 codebook, as a workgroup holds at most 16 waves)
-    if (o.group_tiles || o.mask_mode || o.slice_neurons)
-      return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles, mask_mode and slice_neurons must be 0 for kernel 3");
+    if (o.group_tiles || o.slice_neurons)
+      return fail(SOM_ERR_INVALID_ARG, "opts->group_tiles and slice_neurons must be 0 for kernel 3");
+    if (o.mask_mode < 0 || o.mask_mode > 2) return fail(SOM_ERR_INVALID_ARG, "opts->mask_mode must be 0, 1 or 2");
     const int D = o.tile_docs ? o.tile_docs : 64;
     if (D != 64 && D != 128 && D != 256)
       return fail(SOM_ERR_INVALID_ARG, "opts->tile_docs must be 0, 64, 128 or 256 for kernel 3");
@@ -142,7 +144,11 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, in
     p->T = D == 256 ? 16 : 8;
     p->K = K;
     p->group = D / p->T;
-    p->mask_mode = 1;
+    // SearchArgs encoding for kernel 3: 1 = row-major dispatch, 2 = document-major
+    // (automatic: measured faster on the 128^2, 512^2 and topic workloads); the
+    // document-major form reads its plan's masks stage by stage, per document
+    p->mask_mode = o.mask_mode ? o.mask_mode : 2;
+    p->stage_masks = p->mask_mode == 2;
     p->D = D;
     p->nchunks = (N + 64 * K - 1) / (64 * K);
   } else {
@@ -190,8 +196,9 @@ PlanLayout plan_layout(const Plan& p, int64_t nnz) {
   l.offset = take(o, sizeof(int32_t) * (p.nunits + 1));
   l.count = take(o, sizeof(int32_t) * p.nunits);
   // kernel 3 reads whole stages, and feature ids a few stages ahead, past a
-  // union's end
-  const int64_t pad = p.kernel == 3 ? 256 : 0;
+  // union's end; with stage masks each tile's region is rounded up to whole
+  // 16-entry stages
+  const int64_t pad = p.kernel == 3 ? 256 + (p.stage_masks ? 16 * p.nunits : 0) : 0;
   l.feat = take(o, sizeof(int32_t) * (nnz + pad));
   l.extra = take(o, sizeof(int32_t) * (p.kernel == 3 ? (nnz + pad) * (p.D / 32) : nnz));
   l.total = o;
@@ -248,7 +255,7 @@ hipError_t build_plan(const int32_t* indptr, const int32_t* indices, int64_t B, 
   if (p.kernel == 1 || p.kernel == 3)
     return som::launch_tile_plan(indptr, indices, B, F, perm, static_cast<int>(p.D), at<int32_t>(plan, l.offset),
                                  at<int32_t>(plan, l.count), at<int32_t>(plan, l.feat),
-                                 at<uint32_t>(plan, l.extra), stream);
+                                 at<uint32_t>(plan, l.extra), stream, p.stage_masks);
   return som::launch_group_plan(indptr, indices, B, F, perm, static_cast<int>(p.D),
                                 at<int32_t>(plan, l.offset), at<int32_t>(plan, l.count),
                                 at<int32_t>(plan, l.feat), at<int32_t>(plan, l.extra), stream);

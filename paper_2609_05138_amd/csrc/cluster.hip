@@ -15,7 +15,7 @@
 namespace som {
 namespace {
 
-constexpr int kHistWindow = 16384;   // features per LDS histogram window
+constexpr int kHistWindow = 32768;   // features per LDS histogram window (128 KB)
 constexpr int kHistItems = 1 << 18;  // indices per workgroup
 
 __global__ void __launch_bounds__(256)
@@ -41,32 +41,59 @@ __global__ void k_zero_i32(int32_t* __restrict__ p, int64_t n) {
 
 // Signature key of each document at position d < B: key (s1 << bits) | s2,
 // value d; positions B .. n2-1 are padding that sorts after every document.
+// kSigLanes lanes share a document: each keeps the top two of its share of
+// the features under the order (df descending, id ascending), packed as
+// ((df + 1) << 32) | ~id so that the larger key ranks first (0 = none), and
+// the lanes merge their pairs with shuffles.  Features of a document are
+// distinct, so no two non-empty keys are equal and the merge is exact.
+constexpr int kSigLanes = 8;
+
 __global__ void __launch_bounds__(256)
 k_signature(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, int64_t B, int64_t n2,
             int64_t F, int bits, const int32_t* __restrict__ df, uint64_t* __restrict__ keys,
             uint32_t* __restrict__ vals) {
-  const int64_t d = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (d >= n2) return;
+  const int64_t d = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / kSigLanes;
+  const int sub = threadIdx.x & (kSigLanes - 1);
+  if (d >= n2) return;   // a document's lanes leave together
   if (d >= B) {
-    keys[d] = ~0ull;
-    vals[d] = 0xffffffffu;
+    if (sub == 0) {
+      keys[d] = ~0ull;
+      vals[d] = 0xffffffffu;
+    }
     return;
   }
-  int64_t s1 = F, s2 = F;
-  int32_t c1 = -1, c2 = -1;  // df of s1, s2
-  for (int32_t i = indptr[d]; i < indptr[d + 1]; ++i) {
-    const int64_t f = indices[i];
-    const int32_t c = df[f];
-    // rank by (-df, f); features arrive in ascending f, so "greater df" wins
-    if (c > c1) {
-      s2 = s1; c2 = c1;
-      s1 = f; c1 = c;
-    } else if (c > c2) {
-      s2 = f; c2 = c;
+  uint64_t k1 = 0, k2 = 0;
+  const int32_t e = indptr[d + 1];
+  for (int32_t i = indptr[d] + sub; i < e; i += kSigLanes) {
+    const uint32_t f = static_cast<uint32_t>(indices[i]);
+    const uint64_t k = (static_cast<uint64_t>(df[f] + 1) << 32) | (0xffffffffu - f);
+    if (k > k1) {
+      k2 = k1;
+      k1 = k;
+    } else if (k > k2) {
+      k2 = k;
     }
   }
-  keys[d] = (static_cast<uint64_t>(s1) << bits) | static_cast<uint64_t>(s2);
-  vals[d] = static_cast<uint32_t>(d);
+#pragma unroll
+  for (int off = 1; off < kSigLanes; off <<= 1) {
+    const uint64_t o1 = (static_cast<uint64_t>(__shfl_xor(static_cast<uint32_t>(k1 >> 32), off, kSigLanes)) << 32) |
+                        __shfl_xor(static_cast<uint32_t>(k1), off, kSigLanes);
+    const uint64_t o2 = (static_cast<uint64_t>(__shfl_xor(static_cast<uint32_t>(k2 >> 32), off, kSigLanes)) << 32) |
+                        __shfl_xor(static_cast<uint32_t>(k2), off, kSigLanes);
+    // top two of two ranked pairs: the larger first, then the larger of the
+    // smaller first and both seconds
+    const uint64_t hi = k1 > o1 ? k1 : o1;
+    const uint64_t lo = k1 > o1 ? o1 : k1;
+    const uint64_t s = k2 > o2 ? k2 : o2;
+    k1 = hi;
+    k2 = lo > s ? lo : s;
+  }
+  if (sub == 0) {
+    const int64_t s1 = k1 ? static_cast<int64_t>(0xffffffffu - static_cast<uint32_t>(k1)) : F;
+    const int64_t s2 = k2 ? static_cast<int64_t>(0xffffffffu - static_cast<uint32_t>(k2)) : F;
+    keys[d] = (static_cast<uint64_t>(s1) << bits) | static_cast<uint64_t>(s2);
+    vals[d] = static_cast<uint32_t>(d);
+  }
 }
 
 int key_bits(int64_t F) {
@@ -175,7 +202,7 @@ hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t
   }
   const int bits = key_bits(F);
   const int64_t n2 = cluster_sort_size(B);
-  hipLaunchKernelGGL(k_signature, dim3(static_cast<uint32_t>((n2 + 255) / 256)), dim3(256), 0, stream,
+  hipLaunchKernelGGL(k_signature, dim3(static_cast<uint32_t>((n2 * kSigLanes + 255) / 256)), dim3(256), 0, stream,
                      indptr, indices, B, n2, F, bits, df, keys, vals);
   if (n2 >= 2) {
     const int64_t blk = n2 < kLocal ? n2 : kLocal;

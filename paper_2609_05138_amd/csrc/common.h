@@ -47,10 +47,16 @@ hipError_t launch_validate(const int32_t* indptr, const int32_t* indices, int64_
                            hipStream_t stream);
 
 // Tile plan: tile_offset[ntiles+1] (exclusive scan of per-tile nonzeros),
-// tile_count[ntiles], union_feat / union_mask (see som_tile_plan).
+// tile_count[ntiles], union_feat / union_mask (see som_tile_plan).  With
+// stage_masks (tiles of 64, 128 or 256 documents: the shared-union search's
+// document-major form) each tile's region is rounded up to whole 16-entry
+// stages and each stage's masks are stored document-major: 16-bit word s of
+// the stage (at the stage's first mask word) holds bit r set iff document s
+// holds entry r of the stage.
 hipError_t launch_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                             const int32_t* perm, int T, int32_t* tile_offset, int32_t* tile_count,
-                            int32_t* union_feat, uint32_t* union_mask, hipStream_t stream);
+                            int32_t* union_feat, uint32_t* union_mask, hipStream_t stream,
+                            bool stage_masks = false);
 
 // Document-group plan (for the documents-on-lanes search): per group of D
 // consecutive documents of the tiled order, the sorted feature union and the

@@ -29,9 +29,11 @@ __device__ __forceinline__ int64_t tile_doc(const int32_t* perm, int64_t p) {
   return perm ? static_cast<int64_t>(perm[p]) : p;
 }
 
+// Nonzeros of each tile, rounded up to a multiple of `round` (the space a
+// tile's union may take: |U_t| <= nnz(t)).
 __global__ void __launch_bounds__(256)
 k_tile_nnz(const int32_t* __restrict__ indptr, const int32_t* __restrict__ perm, int64_t B, int T,
-           int64_t ntiles, int32_t* __restrict__ tile_nnz) {
+           int64_t ntiles, int32_t* __restrict__ tile_nnz, int round) {
   const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= ntiles) return;
   int32_t s = 0;
@@ -42,7 +44,7 @@ k_tile_nnz(const int32_t* __restrict__ indptr, const int32_t* __restrict__ perm,
       s += indptr[d + 1] - indptr[d];
     }
   }
-  tile_nnz[t] = s;
+  tile_nnz[t] = (s + round - 1) / round * round;
 }
 
 // Exclusive scan of n values in place into out[0..n] (out[n] = total), one
@@ -241,6 +243,37 @@ k_validate(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indic
   }
 }
 
+// Stage masks of the shared-union search: each tile's union (its region
+// rounded up to whole stages of kStage entries) is cut into stages, and the
+// stage's kStage x T membership bits are rewritten in place from entry-major
+// (entry u: MW words, bit s = document s) to document-major (document s: one
+// 16-bit word, bit r = entry r of the stage; entries past |U_t| are empty).
+// Both forms take 16 * MW words.  One workgroup of T threads per tile, one
+// document per thread; the stage's words pass through LDS, so every read of
+// a stage precedes its rewrite.
+constexpr int kStage = 16;
+
+__global__ void __launch_bounds__(256)
+k_stage_masks(const int32_t* __restrict__ tile_offset, const int32_t* __restrict__ tile_count, int T,
+              uint32_t* __restrict__ union_mask) {
+  __shared__ uint32_t blk[kStage * 8];  // kStage entries x at most 8 words
+  const int MW = T / 32;
+  const int d = threadIdx.x;
+  const int64_t t = blockIdx.x;
+  const int64_t u0 = tile_offset[t];
+  const int32_t cnt = tile_count[t];
+  for (int32_t g = 0; g * kStage < cnt; ++g) {
+    uint32_t* m = union_mask + (u0 + static_cast<int64_t>(g) * kStage) * MW;
+    for (int i = d; i < kStage * MW; i += T) blk[i] = g * kStage + i / MW < cnt ? m[i] : 0u;
+    __syncthreads();
+    uint32_t word = 0u;
+#pragma unroll
+    for (int r = 0; r < kStage; ++r) word |= ((blk[r * MW + (d >> 5)] >> (d & 31)) & 1u) << r;
+    reinterpret_cast<uint16_t*>(m)[d] = static_cast<uint16_t>(word);
+    __syncthreads();
+  }
+}
+
 __global__ void k_fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;
@@ -253,7 +286,7 @@ hipError_t launch_group_plan(const int32_t* indptr, const int32_t* indices, int6
                              int32_t* group_feat, int32_t* entry_pos, hipStream_t stream) {
   const int64_t ngroups = (B + D - 1) / D;
   hipLaunchKernelGGL(k_tile_nnz, dim3(static_cast<uint32_t>((ngroups + 255) / 256)), dim3(256), 0,
-                     stream, indptr, perm, B, D, ngroups, group_count);
+                     stream, indptr, perm, B, D, ngroups, group_count, 1);
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, group_count, ngroups, group_offset);
   const int window = static_cast<int>(F < kPlanWindow ? F : kPlanWindow);
   const size_t lds = sizeof(uint32_t) * static_cast<size_t>(window);
@@ -282,11 +315,12 @@ hipError_t launch_validate(const int32_t* indptr, const int32_t* indices, int64_
 
 hipError_t launch_tile_plan(const int32_t* indptr, const int32_t* indices, int64_t B, int64_t F,
                             const int32_t* perm, int T, int32_t* tile_offset, int32_t* tile_count,
-                            int32_t* union_feat, uint32_t* union_mask, hipStream_t stream) {
+                            int32_t* union_feat, uint32_t* union_mask, hipStream_t stream, bool stage_masks) {
   const int64_t ntiles = (B + T - 1) / T;
+  if (stage_masks && (T < 64 || T > 256 || T % 32 != 0)) return hipErrorInvalidValue;
   // per-tile nonzeros are staged in tile_count, then scanned into tile_offset
   hipLaunchKernelGGL(k_tile_nnz, dim3(static_cast<uint32_t>((ntiles + 255) / 256)), dim3(256), 0,
-                     stream, indptr, perm, B, T, ntiles, tile_count);
+                     stream, indptr, perm, B, T, ntiles, tile_count, stage_masks ? kStage : 1);
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, tile_count, ntiles, tile_offset);
   const int MW = (T + 31) / 32;
   const int window = static_cast<int>(F < kPlanWindow / MW ? F : kPlanWindow / MW);
@@ -298,6 +332,9 @@ hipError_t launch_tile_plan(const int32_t* indptr, const int32_t* indices, int64
   hipLaunchKernelGGL(k_plan, dim3(static_cast<uint32_t>(ntiles)), dim3(kPlanThreads), lds, stream,
                      indptr, indices, perm, B, F, T, MW, window, tile_offset, tile_count, union_feat,
                      union_mask);
+  if (stage_masks)
+    hipLaunchKernelGGL(k_stage_masks, dim3(static_cast<uint32_t>(ntiles)), dim3(static_cast<uint32_t>(T)), 0,
+                       stream, tile_offset, tile_count, T, union_mask);
   return hipGetLastError();
 }
 

@@ -78,7 +78,20 @@ __device__ __forceinline__ void wait_stages(int n) {
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <typename WT, int T, int K, int S, int P, int NSLOT>
+// Dispatch of a stage's rows to a wave's documents (both add every row in
+// ascending feature order, so their results are bit-identical):
+//   kStRowMajor: visit each entry some document of the wave holds (one
+//     ballot over the stage's entry-major masks), read its row from LDS once,
+//     then a scalar branch tree over the wave's documents (a test per group
+//     of four, then one per document);
+//   kStDocMajor: the plan stores each stage's masks document-major (one
+//     16-bit word per document: the stage entries it holds); the wave's T
+//     words arrive in scalar registers with one scalar load issued a stage
+//     ahead, and per document each held entry is read from LDS and added,
+//     with a static accumulator index and no per-row scalar branch tree.
+enum StDispatch { kStRowMajor = 0, kStDocMajor = 1 };
+
+template <typename WT, int T, int K, int S, int P, int NSLOT, int DISP>
 __global__ void __launch_bounds__(S * 64)
 k_search_st(SearchArgs a) {
   constexpr int E = Storage<WT>::kE;  // elements per 128-bit load
@@ -137,6 +150,18 @@ k_search_st(SearchArgs a) {
               : a.union_mask + (static_cast<int64_t>(u0) + (lane & (P - 1))) * MW + mword;
   const int64_t dstride = id_lane ? P : static_cast<int64_t>(P) * MW;  // words per stage
   const int32_t nstages = (cnt + P - 1) / P;
+  // document-major stage masks (P = 16 entries per stage): stage q's word of
+  // document j is 16-bit word j at mask word (u0 + q * P) * MW; this wave's
+  // T words are T / 2 consecutive 32-bit words
+  typedef const __attribute__((address_space(4))) uint32_t* const_u32;
+  const const_u32 smask = (const_u32)(a.union_mask + static_cast<int64_t>(u0) * MW) + wave * (T / 2);
+  constexpr int SW = T / 2;   // 32-bit words of stage masks per wave and stage
+  uint32_t dmw[SW];
+  if (DISP == kStDocMajor) {
+    static_assert(P == 16, "document-major stage masks hold 16 entries");
+#pragma unroll
+    for (int k = 0; k < SW; ++k) dmw[k] = nstages > 0 ? smask[k] : 0u;
+  }
   const uint32_t ring0 = lds_offset(&ring[0][0][0]) + static_cast<uint32_t>(wave * RPW * 1024);
   const uint32_t mring0 = lds_offset(&mring[0][0][0]) + static_cast<uint32_t>(wave * 256);
 
@@ -171,10 +196,59 @@ k_search_st(SearchArgs a) {
       const int slot = s % NSLOT;
       const uint32_t w = mring[slot][wave][lane];
       if (s + NSLOT - 1 < nstages) {
-        int32_t fid[RPW];
+        const int32_t q = s + NSLOT - 1;
+        if (DISP == kStDocMajor) {
+          // byte offsets of stage q's rows, computed once on the id lanes
+          // (lane P + r holds entry r's feature id; past the union: row 0),
+          // then moved to scalar registers one row at a time
+          const bool live = id_lane && q * P + (lane - P) < cnt;
+          const uint64_t off = static_cast<uint64_t>(live ? w : 0u) * static_cast<uint64_t>(ldw_b);
+          const uint32_t slot_ = static_cast<uint32_t>(q % NSLOT);
 #pragma unroll
-        for (int i = 0; i < RPW; ++i) fid[i] = __builtin_amdgcn_readlane(static_cast<int>(w), P + wave * RPW + i);
-        SOM_ST_ISSUE(s + NSLOT - 1, fid)
+          for (int i = 0; i < RPW; ++i) {
+            const int src = P + wave * RPW + i;
+            const uint64_t o = (static_cast<uint64_t>(static_cast<uint32_t>(
+                                   __builtin_amdgcn_readlane(static_cast<int>(off >> 32), src))) << 32) |
+                               static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), src));
+            dma_b128(Wn + o, ring0 + slot_ * (P * 1024) + static_cast<uint32_t>(i * 1024));
+          }
+          dma_b32(dsrc + q * dstride, mring0 + slot_ * (S * 256));
+        } else {
+          int32_t fid[RPW];
+#pragma unroll
+          for (int i = 0; i < RPW; ++i) fid[i] = __builtin_amdgcn_readlane(static_cast<int>(w), P + wave * RPW + i);
+          SOM_ST_ISSUE(q, fid)
+        }
+      }
+      if (DISP == kStDocMajor) {
+        uint32_t cur[SW];
+#pragma unroll
+        for (int k = 0; k < SW; ++k) cur[k] = dmw[k];
+#pragma unroll
+        for (int sd = 0; sd < T; ++sd) {
+          // the entries of stage s that document sd of this wave holds
+          uint32_t dm = (cur[sd >> 1] >> ((sd & 1) * 16)) & 0xffffu;
+          while (dm) {
+            const int r = __builtin_ctz(dm);
+            dm &= dm - 1;
+            float4 wf[K / 4];
+            widen_v<WT>(ring[slot][r][lane], wf);
+#pragma unroll
+            for (int qq = 0; qq < K / 4; ++qq) {
+              acc[sd][4 * qq + 0] += wf[qq].x;
+              acc[sd][4 * qq + 1] += wf[qq].y;
+              acc[sd][4 * qq + 2] += wf[qq].z;
+              acc[sd][4 * qq + 3] += wf[qq].w;
+            }
+          }
+        }
+        // the next stage's words, loaded now (their wait falls on the next
+        // stage's first LDS read, after its barrier)
+        if (s + 1 < nstages) {
+#pragma unroll
+          for (int k = 0; k < SW; ++k) dmw[k] = smask[(s + 1) * P * MW + k];
+        }
+        continue;
       }
       const uint32_t m_cur = (lane < P && s * P + lane < cnt) ? (w >> mshift) & kWaveBits : 0u;
       // this wave's needed entries of stage s, visited in ascending order
@@ -208,6 +282,7 @@ k_search_st(SearchArgs a) {
 
 template <typename WT, int T, int K, int S>
 hipError_t launch_st(const SearchArgs& a, hipStream_t stream) {
+  // mask_mode: 1 = row-major dispatch, 2 = document-major
   // 16-entry stages in a ring of two: 32 KB of rows per workgroup, so four
   // workgroups of eight 8-document waves share a CU.  Measured on the 512^2
   // map (fp32, 262,144 documents): the number of waves a CU can interleave
@@ -217,7 +292,10 @@ hipError_t launch_st(const SearchArgs& a, hipStream_t stream) {
   constexpr int P = 16;
   constexpr int NSLOT = 2;
   const dim3 grid(static_cast<uint32_t>((a.ntiles + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));
-  hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT>), grid, dim3(S * 64), 0, stream, a);
+  if (a.mask_mode == 2)
+    hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT, kStDocMajor>), grid, dim3(S * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT, kStRowMajor>), grid, dim3(S * 64), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -159,7 +159,7 @@ def test_search_rejects_bad_arguments(lib):
     res = som.som_bmu_opts()
     res.storage = 2
     O = som.som_bmu_opts
-    for bad in (O(4), O(-1), O(3, 32), O(3, 16), O(3, 0, 8), O(3, 0, 0, 2), O(3, 0, 0, 0, 1), O(3, 0, 0, 0, 0, 32),
+    for bad in (O(4), O(-1), O(3, 32), O(3, 16), O(3, 0, 8), O(3, 0, 0, 2), O(3, 0, 0, 0, 3), O(3, 0, 0, 0, 0, 32),
                 O(1, 5), O(1, 0, 3), res, O(1, 0, 0, 16), O(1, 0, 0, 0, 3), O(1, 32, 8),
                 O(0, 0, 0, 0, 0, 0, 2), O(1, 0, 0, -1), O(2, 8), O(2, 0, 4), O(2, 0, 0, 1),
                 O(2, 0, 0, 0, 1), O(2, 0, 0, 0, 0, 48), O(1, 0, 0, 0, 0, 32)):

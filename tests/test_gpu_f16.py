@@ -31,7 +31,8 @@ DEV = "cuda:0"
 REL = 1e-5
 KNOBS16 = [dict(), dict(tile_docs=1), dict(tile_docs=4), dict(tile_docs=16), dict(group_tiles=4),
            dict(mask_mode=1), dict(kernel=1, lane_neurons=8, group_tiles=2),
-           dict(kernel=3), dict(kernel=3, tile_docs=128)]
+           dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, mask_mode=2),
+           dict(kernel=3, tile_docs=128, mask_mode=2)]
 
 
 def _csr(docs):

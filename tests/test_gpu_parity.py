@@ -109,7 +109,8 @@ def test_norms_dyadic_bit_exact():
 
 @pytest.mark.parametrize("knobs", [dict(kernel=1, tile_docs=T) for T in TILES]
                          + [dict(kernel=2, group_tiles=G, slice_neurons=NB) for G in (4, 16) for NB in (32, 64)]
-                         + [dict(kernel=3, tile_docs=D) for D in SUPER])
+                         + [dict(kernel=3, tile_docs=D) for D in SUPER]
+                         + [dict(kernel=3, tile_docs=D, mask_mode=2) for D in SUPER])
 def test_hand_examples_bit_exact(knobs):
     ex_all = json.load(open(os.path.join(GOLDEN, "hand_examples.json")))["examples"]
     for ex in ex_all:
@@ -142,7 +143,8 @@ def test_dyadic_codebook_bit_exact_with_ties(N):
     exact = oracle.bmu_search_exact(K, 2, indptr, indices)
     for knobs in (dict(kernel=1, tile_docs=1), dict(kernel=1, tile_docs=8), dict(kernel=1, tile_docs=32),
                   dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64),
-                  dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256)):
+                  dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256),
+                  dict(kernel=3, mask_mode=2), dict(kernel=3, tile_docs=256, mask_mode=2)):
         bmu, dist, _ = _search(W, indptr, indices, **knobs)
         assert bmu.tolist() == [e[2][0] for e in exact]
         assert [Fraction(float(x)) for x in dist] == [Fraction(e[1], 16) for e in exact]
@@ -294,7 +296,7 @@ def test_results_identical_across_tile_chunk_and_order():
     for T in TILES:
         for K, G, mode in ((0, 0, 0), (4, 1, 1), (8 if T < 32 else 4, 8, 2), (4, 2, 2)):
             variants.append(dict(kernel=1, tile_docs=T, lane_neurons=K, group_tiles=G, mask_mode=mode))
-    variants += [dict(kernel=3, tile_docs=D) for D in SUPER]
+    variants += [dict(kernel=3, tile_docs=D, mask_mode=m) for D in SUPER for m in (1, 2)]
     for i, v in enumerate(variants):
         for perm in perms if (i % 5 == 0 or v["kernel"] == 3) else perms[:2]:
             out = _search(W, indptr, indices, perm=perm, **v)
