@@ -77,9 +77,8 @@ def parse(argv=None):
     p.add_argument("--batch", type=int, default=-1, help="one batch of the pass instead of all (-1)")
     p.add_argument("--docs", type=int, default=0, help="with --batch: the first DOCS documents only")
     p.add_argument("--ldw", type=int, default=0, help="codebook row stride in floats (0 = recommended)")
-    p.add_argument("--kernel", type=int, default=-1,
-                   help="0 library auto (kernel 1), 1, 2 or 3; -1 = 3 for the 128^2 map and the topic "
-                        "workload (fp32), else the library's choice")
+    p.add_argument("--kernel", type=int, default=0,
+                   help="0 = the library's automatic choice (kernel 3 for fp32, kernel 1 for fp16), 1, 2 or 3")
     p.add_argument("--tile-docs", type=int, default=0)
     p.add_argument("--lane-neurons", type=int, default=0)
     p.add_argument("--group-tiles", type=int, default=0)
@@ -114,15 +113,11 @@ def log(args, *a):
 
 
 def launch_knobs(args, cfg):
-    """Search knobs of the timed launch (0 = the library's automatic choice).
-
-    The library resolves kernel 1's tile size and tiles per workgroup from N
-    and the storage type.  What it cannot see is the data: for the 128^2 map
-    and the topic workload (no global head) kernel 3's 64-document
-    super-tiles were measured faster, so the benchmark asks for them there."""
-    kernel = args.kernel
-    if kernel < 0:
-        kernel = 3 if (cfg.key in (2, 5) and args.weights == "f32" and not args.unfused) else 0
+    """Search knobs of the timed launch: 0 everywhere unless given, i.e. the
+    library's automatic launch (it resolves the kernel, tile size and tiles
+    per workgroup from N and the storage type); the unfused comparator is
+    built on kernel 1."""
+    kernel = args.kernel or (1 if args.unfused else 0)
     return dict(kernel=kernel, tile_docs=args.tile_docs, lane_neurons=args.lane_neurons,
                 group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons,
                 storage=1 if args.weights == "f16" else 0)
@@ -172,6 +167,19 @@ def _oracle_job(job):
     return b, docs, res, time.perf_counter() - t
 
 
+class _InProcess:
+    """Pool stand-in that runs the jobs in this process."""
+
+    def map(self, fn, jobs, chunksize=1):
+        return [fn(j) for j in jobs]
+
+    def close(self):
+        pass
+
+    def join(self):
+        pass
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -203,11 +211,11 @@ def main():
     # ---- host inputs (before any GPU call) ----
     t = time.time()
     jobs = [(cfg.key, b, args.docs or None) for b in batches]
-    if len(jobs) > 1:
+    if len(jobs) > 1 and procs > 1:
         with ctx.Pool(min(procs, len(jobs))) as pool:
             docs = dict(zip(batches, pool.map(_gen_batch, jobs, chunksize=1)))
     else:
-        docs = {batches[0]: _gen_batch(jobs[0])}
+        docs = {b: _gen_batch(j) for b, j in zip(batches, jobs)}
     sizes = [len(docs[b][0]) - 1 for b in batches]
     nnzs = [len(docs[b][1]) for b in batches]
     log(args, f"{len(batches)} batch(es), {sum(sizes)} documents, nnz={sum(nnzs)} generated in "
@@ -221,7 +229,9 @@ def main():
     pool = None
     if sample:
         _HOST.update(W=W_or, norms64=norms64, batches=docs)
-        pool = ctx.Pool(procs)
+        # with one process (e.g. under a profiler, which initialises the GPU
+        # before the program starts) nothing is forked: the oracle runs here
+        pool = ctx.Pool(procs) if procs > 1 else _InProcess()
 
     # ---- device ----
     import torch
@@ -245,27 +255,27 @@ def main():
         torch.cuda.empty_cache()
     del Wh
     knobs = launch_knobs(args, cfg)
-    kernel = knobs["kernel"] or 1
-    if args.unfused and (args.weights != "f32" or args.top2 or kernel != 1 or args.stream):
+    if args.unfused and (args.weights != "f32" or args.top2 or knobs["kernel"] != 1 or args.stream):
         raise SystemExit("--unfused runs the fp32, kernel-1, best-unit, resident search only")
     o_auto = som.som._opts(**knobs)
     lib = som.load()
 
-    # the tile geometry the library resolves for this launch (read back
-    # through som_plan_bytes, so the benchmark never restates the rule)
+    # the kernel and tile geometry the library resolves for this launch (read
+    # back through som_plan_bytes, so the benchmark never restates the rule)
     Bmax, nnzmax = max(sizes), max(nnzs)
     plan_need = int(lib.som_plan_bytes(Bmax, nnzmax, ctypes.byref(o_auto)))
-    cands = (64, 128, 256) if kernel == 3 else ((1, 2, 4, 8, 16, 32) if kernel == 1 else ())
-    unit_docs = None
-    for T in cands:
-        o = som.som._opts(**dict(knobs, tile_docs=T))
-        if int(lib.som_plan_bytes(Bmax, nnzmax, ctypes.byref(o))) == plan_need:
-            unit_docs = T
-            break
-    if kernel == 2:
-        unit_docs = 64 * (args.group_tiles or 16)
-    if unit_docs is None:
-        raise SystemExit("could not resolve the launch's tile size")
+    if knobs["kernel"] == 2:
+        kernel, unit_docs = 2, 64 * (args.group_tiles or 16)
+    else:
+        kernels = (knobs["kernel"],) if knobs["kernel"] else (3, 1)
+        cands = [(k, T) for k in kernels for T in ((64, 128, 256) if k == 3 else (1, 2, 4, 8, 16, 32))]
+        match = [(k, T) for k, T in cands
+                 if int(lib.som_plan_bytes(Bmax, nnzmax, ctypes.byref(som.som._opts(**dict(knobs, kernel=k,
+                                                                                          tile_docs=T)))))
+                 == plan_need]
+        if not match:
+            raise SystemExit("could not resolve the launch's kernel and tile size")
+        kernel, unit_docs = match[0]
 
     norms = torch.empty(N, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()

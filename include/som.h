@@ -57,13 +57,16 @@ typedef enum som_status {
  * is summed in ascending feature order whatever the knobs, so outputs are
  * bit-identical across all settings.
  *
- * Automatic choices (measured on the 512^2 and 256^2 maps, F = 20,000,
- * 1M-document batches): kernel 1; tiles of 16 documents for an fp32
- * codebook and 8 for fp16; four tiles per workgroup for fp32 tiles of 16
- * documents when N >= 131,072, one otherwise.  The automatic tile size
- * depends on the storage type: a search that plans internally uses its own
- * (fp32 or fp16); som_plan, som_plan_bytes and the planned searches use
- * opts->storage, so a plan and its search always agree on the geometry.
+ * Automatic choices (measured on MI355X at map sizes 32^2 to 512^2, F =
+ * 2,048 to 20,000, batches up to 1M documents): for an fp32 codebook kernel
+ * 3 with 64-document super-tiles and the document-major dispatch; for fp16,
+ * or when a knob only kernel 1 has is set (tile_docs of 32 or less,
+ * lane_neurons, group_tiles), kernel 1 with tiles of 16 documents for fp32
+ * and 8 for fp16, and four tiles per workgroup for fp32 tiles of 16
+ * documents when N >= 131,072.  The automatic choices depend on the storage
+ * type: a search that plans internally uses its own (fp32 or fp16);
+ * som_plan, som_plan_bytes and the planned searches use opts->storage, so a
+ * plan and its search always agree on the geometry.
  *
  * kernel 1, neurons on lanes: a wave holds a tile of T documents (Section
  *   4.1) against 64*K neurons (K per lane, 128-bit loads, Section 4.3) and
@@ -85,7 +88,7 @@ typedef enum som_status {
  * Every kernel cuts the neuron axis into slices whose minima are merged
  * (Section 4.2) and fuses the argmin (Section 3). */
 typedef struct som_bmu_opts {
-  int32_t kernel;        /* 0 = auto (kernel 1), 1 = neurons on lanes, 2 = documents on lanes,
+  int32_t kernel;        /* 0 = auto (see above), 1 = neurons on lanes, 2 = documents on lanes,
                             3 = shared-union super-tiles */
   int32_t tile_docs;     /* kernel 1: T = 0 (auto: 16 for fp32, 8 for fp16), 1, 2, 4, 8, 16 or 32;
                             kernel 3: D = 0 (auto: 64), 64, 128 or 256 (256: fp32 only) */
@@ -337,8 +340,8 @@ som_status som_bmu_search_top2_planned_f16(const uint16_t* W, int64_t F, int64_t
  * of block_docs documents at a time (fp32 [block_docs][N], in ws), then one
  * wave per document reduces its row.  The distances are the fused search's
  * fp32 values, so bmu and dist are bit-identical to som_bmu_search's with the
- * same opts.  Kernel 1 and an fp32 codebook only; block_docs a positive
- * multiple of the tile size.  ws: som_bmu_search_unfused_workspace_bytes
+ * same opts.  Kernel 1 (also when opts->kernel is 0) and an fp32 codebook
+ * only; block_docs a positive multiple of the tile size.  ws: som_bmu_search_unfused_workspace_bytes
  * (plan + score block). */
 size_t som_bmu_search_unfused_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
                                               const som_bmu_opts* opts, int64_t block_docs);

@@ -103,7 +103,12 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, in
   if (o.storage != 0 && o.storage != 1) return fail(SOM_ERR_INVALID_ARG, "opts->storage must be 0 (fp32) or 1 (fp16)");
   if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
   if (o.kernel < 0 || o.kernel > 3) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1, 2 or 3");
-  const int kernel = o.kernel ? o.kernel : 1;
+  // automatic kernel: the shared-union super-tiles (kernel 3) for an fp32
+  // codebook, measured faster at every map size from 32^2 to 512^2 and on the
+  // topic workload; kernel 1 for fp16 (8-document tiles, measured faster
+  // there) and whenever a knob only kernel 1 has is given
+  const bool k1_knob = (o.tile_docs > 0 && o.tile_docs <= 32) || o.lane_neurons || o.group_tiles;
+  const int kernel = o.kernel ? o.kernel : ((auto16 || k1_knob) ? 1 : 3);
   p->kernel = kernel;
   if (kernel == 1) {
     // automatic tile size: 16 documents for fp32 (about 5% faster than 8 on
@@ -709,7 +714,11 @@ static UnfusedWs unfused_ws(const Plan& p, int64_t N, int64_t nnz, int64_t block
 }
 
 static som_status unfused_plan(int64_t N, int64_t B, const som_bmu_opts* opts, int64_t block_docs, Plan* p) {
-  som_status s = make_plan(N, B, opts, p, som::kWeightsF32, som::kWeightsF32);
+  // the comparator is built on kernel 1: the automatic kernel resolves to it
+  som_bmu_opts o{};
+  if (opts) o = *opts;
+  if (o.kernel == 0) o.kernel = 1;
+  som_status s = make_plan(N, B, &o, p, som::kWeightsF32, som::kWeightsF32);
   if (s != SOM_OK) return s;
   if (p->kernel != 1) return fail(SOM_ERR_INVALID_ARG, "the unfused comparator uses kernel 1");
   if (opts && opts->validate) return fail(SOM_ERR_INVALID_ARG, "validate is not available on the unfused comparator");

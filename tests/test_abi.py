@@ -45,25 +45,30 @@ def test_abi_version(lib):
     assert som.som_abi_version() == 12
 
 
-def test_automatic_tile_size_follows_the_storage_type(lib):
-    # som_plan resolves the automatic tile size from opts->storage: 16
-    # documents for fp32, 8 for fp16 (twice the tiles, so larger per-tile
-    # arrays); explicit sizes do not depend on it
+def test_automatic_launch_follows_the_storage_type(lib):
+    # som_plan resolves the automatic launch from opts->storage: kernel 3 with
+    # 64-document super-tiles for fp32, kernel 1 with 8-document tiles for
+    # fp16; a knob only kernel 1 has (here 16-document tiles) selects kernel 1
     B, nnz = 1 << 20, 84_000_000
-    f32, f16 = som.som_bmu_opts(), som.som_bmu_opts()
-    f16.storage = 1
-    p32 = lib.som_plan_bytes(B, nnz, ctypes.byref(f32))
-    p16 = lib.som_plan_bytes(B, nnz, ctypes.byref(f16))
-    assert p16 - p32 >= 8 * (B // 8 - B // 16)
-    t8, t8h = som.som_bmu_opts(1, 8), som.som_bmu_opts(1, 8)
-    t8h.storage = 1
-    assert lib.som_plan_bytes(B, nnz, ctypes.byref(t8)) == lib.som_plan_bytes(B, nnz, ctypes.byref(t8h)) == p16
+    O = som.som_bmu_opts
+
+    def plan_bytes(o, storage=0):
+        o.storage = storage
+        return lib.som_plan_bytes(B, nnz, ctypes.byref(o))
+
+    p32, p16 = plan_bytes(O()), plan_bytes(O(), 1)
+    assert p32 == plan_bytes(O(3, 64)) and p32 != plan_bytes(O(1, 16))
+    assert p16 == plan_bytes(O(1, 8), 1) == plan_bytes(O(1, 8))
+    assert plan_bytes(O(0, 16)) == plan_bytes(O(1, 16))
+    assert plan_bytes(O(0, 0, 0, 4)) == plan_bytes(O(1, 16))       # group_tiles: kernel 1, 16-document tiles
     # a search that plans internally may be either storage type: its
-    # workspace covers the larger (fp16) automatic plan
-    assert lib.som_bmu_workspace_bytes(20000, 262144, B, nnz, None) >= p16 + 8 * B
+    # workspace covers the larger automatic plan
+    assert lib.som_bmu_workspace_bytes(20000, 262144, B, nnz, None) >= max(p32, p16) + 8 * B
     # the planned workspace holds keys only
+    f16 = O()
+    f16.storage = 1
     assert (lib.som_bmu_search_planned_workspace_bytes(262144, B, ctypes.byref(f16))
-            == lib.som_bmu_search_planned_workspace_bytes(262144, B, ctypes.byref(f32)))
+            == lib.som_bmu_search_planned_workspace_bytes(262144, B, ctypes.byref(O())))
 
 
 def test_probe_rejects_bad_arguments(lib):

@@ -41,15 +41,16 @@ def test_help_lists_the_contract_flags():
 
 
 def test_default_launch_leaves_the_knobs_to_the_library():
-    # the measured launch lives in the library (automatic tile size and tiles
-    # per workgroup); the benchmark asks only for kernel 3 where the data, which
-    # the library cannot see, favours it (128^2 map, topic workload)
+    # the measured launch lives in the library (automatic kernel, tile size
+    # and tiles per workgroup from N and the storage type): the benchmark
+    # passes no knob, except kernel 1 for the unfused comparator built on it
     sys.path.insert(0, ROOT)
     import bench
     from synth import CONFIGS
     for argv, cfg_key, kernel, storage in ((["--config", "4"], 4, 0, 0), (["--weights", "f16"], 4, 0, 1),
-                                           (["--config", "3"], 3, 0, 0), (["--config", "5"], 5, 3, 0),
-                                           (["--config", "2"], 2, 3, 0), (["--config", "5", "--weights", "f16"], 5, 0, 1)):
+                                           (["--config", "3"], 3, 0, 0), (["--config", "5"], 5, 0, 0),
+                                           (["--config", "2"], 2, 0, 0), (["--config", "5", "--weights", "f16"], 5, 0, 1),
+                                           (["--unfused"], 4, 1, 0)):
         knobs = bench.launch_knobs(bench.parse(argv), CONFIGS[cfg_key])
         assert knobs.pop("kernel") == kernel and knobs.pop("storage") == storage, argv
         assert not any(knobs.values()), (argv, knobs)

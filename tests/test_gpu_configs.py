@@ -6,9 +6,10 @@ batch of the pass, each batch's first and last document included; for the
 26.9M-document topic pass (27 batches) its first, middle and last batch with
 about 2,048 documents between them (the whole pass, all 27 batches, is
 checked by the benchmark's pass mode).  Each batch is searched in the
-launch configuration the benchmark uses (the library's automatic knobs for
-kernel 1; kernel 3 with 64-document super-tiles for the 128^2 map and the
-topic workload; codebook rows at the recommended stride) and checked:
+launch configuration the benchmark uses (the library's automatic launch:
+kernel 3 with 64-document super-tiles for an fp32 codebook, kernel 1 with
+8-document tiles for fp16; codebook rows at the recommended stride) and
+checked:
   * sampled documents against the fp64 oracle under the acceptance rule
     (device index equal to the oracle's BMU or inside its 1e-5 near-tie
     band; device distance within 1e-5 relative), the oracle sharded over
@@ -134,14 +135,13 @@ def _host(*ts):
 
 
 def test_config2_every_document_of_the_first_batch():
-    # 128^2 map: the benchmark searches it with kernel 3 (64-document
-    # super-tiles) on the clustered order; kernel 1 with the automatic knobs
-    # must give the same bits
+    # 128^2 map, the automatic launch (kernel 3, 64-document super-tiles) on
+    # the clustered order; kernel 1 must give the same bits
     P = _Pass(2)
     indptr, indices, ip, ix = P.batch(0)
     perm = som.som_cluster_order(ip, ix, P.cfg.F)
-    bmu, dist = P.search(ip, ix, perm, kernel=3)
-    b1, d1 = P.search(ip, ix, perm)
+    bmu, dist = P.search(ip, ix, perm)
+    b1, d1 = P.search(ip, ix, perm, kernel=1)
     assert torch.equal(b1, bmu) and torch.equal(d1, dist), "kernel 1 differs from kernel 3"
     bmu, dist = _host(bmu, dist)
     B = len(indptr) - 1
@@ -152,7 +152,7 @@ def test_config2_every_document_of_the_first_batch():
 
 def test_config3_sample_over_every_batch():
     # 256^2 map, 4,000,000 documents in four batches (the last 854,272):
-    # 512 sampled documents per batch, automatic kernel-1 launch, input order
+    # 512 sampled documents per batch, automatic launch, input order
     from synth import batch_sizes
     P = _Pass(3)
     nb = len(batch_sizes(P.cfg))
@@ -160,9 +160,9 @@ def test_config3_sample_over_every_batch():
     for b in range(nb):
         indptr, indices, ip, ix = P.batch(b)
         bmu, dist = P.search(ip, ix, None)
-        if b == nb - 1:   # kernel 3 sums in the same order: the same bits on a whole batch
-            b3, d3 = P.search(ip, ix, None, kernel=3)
-            assert torch.equal(b3, bmu) and torch.equal(d3, dist), "kernel 3 differs from kernel 1"
+        if b == nb - 1:   # kernel 1 sums in the same order: the same bits on a whole batch
+            b3, d3 = P.search(ip, ix, None, kernel=1)
+            assert torch.equal(b3, bmu) and torch.equal(d3, dist), "kernel 1 differs from kernel 3"
             del b3, d3
         bmu, dist = _host(bmu, dist)
         _distance_property(P.W, P.norms64, indptr, indices, bmu.astype(np.int64), dist.astype(np.float64))
@@ -175,10 +175,11 @@ def test_config3_sample_over_every_batch():
 
 def test_config4_sample_over_both_batches():
     # 512^2 map, 2,000,000 documents in two batches (1,048,576 + 951,424),
-    # clustered, automatic launch (16-document tiles, four per workgroup):
-    # 1,024 sampled documents per batch.  Batch 0 also checks one tile per
-    # workgroup and kernel 3 for identical bits, the top-2 search (same
-    # first place, second place against the oracle) and the fp16 codebook.
+    # clustered, automatic launch (kernel 3): 1,024 sampled documents per
+    # batch.  Batch 0 also checks kernel 1 (16-document tiles, four and one
+    # per workgroup) for identical bits, the top-2 search (same first place,
+    # second place against the oracle) and the fp16 codebook (automatic:
+    # kernel 1, 8-document tiles; kernel 3 for identical bits).
     P = _Pass(4)
     bad = []
     for b in (0, 1):
@@ -190,9 +191,9 @@ def test_config4_sample_over_both_batches():
         half = None
         if b == 0:
             b1, d1 = P.search(ip, ix, perm, group_tiles=1)
-            assert torch.equal(b1, bmu) and torch.equal(d1, dist), "one tile per workgroup differs"
-            b3, d3 = P.search(ip, ix, perm, kernel=3)
-            assert torch.equal(b3, bmu) and torch.equal(d3, dist), "kernel 3 differs from kernel 1"
+            assert torch.equal(b1, bmu) and torch.equal(d1, dist), "kernel 1, one tile per workgroup, differs"
+            b3, d3 = P.search(ip, ix, perm, kernel=1)
+            assert torch.equal(b3, bmu) and torch.equal(d3, dist), "kernel 1 differs from kernel 3"
             del b1, d1, b3, d3
             t2 = som.som_bmu_search_top2(P.Wd, P.norms, ip, ix, N=P.cfg.N, perm=perm)
             assert torch.equal(t2[0], bmu) and torch.equal(t2[1], dist)
@@ -223,16 +224,16 @@ def test_config4_sample_over_both_batches():
 
 def test_config5_first_middle_and_last_batches():
     # topic workload, 27 batches of 1,000,000 documents (the last 900,000):
-    # batches 0, 13 and 26, clustered, kernel 3 with 64-document super-tiles
-    # (the benchmark's choice); batch 26 also runs kernel 1 for identical bits
+    # batches 0, 13 and 26, clustered, automatic launch (kernel 3 with
+    # 64-document super-tiles); batch 26 also runs kernel 1 for identical bits
     P = _Pass(5)
     bad = []
     for b in (0, 13, 26):
         indptr, indices, ip, ix = P.batch(b)
         perm = som.som_cluster_order(ip, ix, P.cfg.F)
-        bmu, dist = P.search(ip, ix, perm, kernel=3)
+        bmu, dist = P.search(ip, ix, perm)
         if b == 26:
-            b1, d1 = P.search(ip, ix, perm)
+            b1, d1 = P.search(ip, ix, perm, kernel=1)
             assert torch.equal(b1, bmu) and torch.equal(d1, dist), "kernel 1 differs from kernel 3"
             del b1, d1
         bmu, dist = _host(bmu, dist)
