@@ -104,6 +104,10 @@ typedef struct som_bmu_opts {
   int32_t storage;       /* 0 = fp32, 1 = fp16: the codebook storage type whose automatic tile
                             size som_plan, som_plan_bytes and the planned searches resolve
                             (searches that plan internally use their own type) */
+  int32_t schedule;      /* kernel 3: 0 = auto (1), 1 = one launch over every neuron slice,
+                            2 = round-synchronised launches: per slice, one launch per round of
+                            as many super-tiles as the device holds at once, so that they sweep
+                            their ascending unions side by side; kernels 1 and 2: 0 or 1 */
 } som_bmu_opts;
 
 /* Version of this ABI (bumped on any incompatible change). */

@@ -81,6 +81,7 @@ struct Plan {
   int64_t nunits = 0;   // tiles or groups
   int64_t nchunks = 0;  // neuron slices
   bool stage_masks = false;  // kernel 3, document-major: masks stored per stage and document
+  int schedule = 1;          // 1 = one launch, 2 = round-synchronised launches (kernel 3)
 };
 
 // Kernel-1 tiles per workgroup chosen automatically: four consecutive tiles
@@ -102,6 +103,7 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, in
   if (f16 && o.kernel == 2) return fail(SOM_ERR_INVALID_ARG, "an fp16 codebook is searched by kernels 1 and 3 only");
   if (o.storage != 0 && o.storage != 1) return fail(SOM_ERR_INVALID_ARG, "opts->storage must be 0 (fp32) or 1 (fp16)");
   if (o.validate != 0 && o.validate != 1) return fail(SOM_ERR_INVALID_ARG, "opts->validate must be 0 or 1");
+  if (o.schedule < 0 || o.schedule > 2) return fail(SOM_ERR_INVALID_ARG, "opts->schedule must be 0, 1 or 2");
   if (o.kernel < 0 || o.kernel > 3) return fail(SOM_ERR_INVALID_ARG, "opts->kernel must be 0, 1, 2 or 3");
   // automatic kernel: the shared-union super-tiles (kernel 3) for an fp32
   // codebook, measured faster at every map size from 32^2 to 512^2 and on the
@@ -154,6 +156,7 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, in
     // document-major form reads its plan's masks stage by stage, per document
     p->mask_mode = o.mask_mode ? o.mask_mode : 2;
     p->stage_masks = p->mask_mode == 2;
+    p->schedule = o.schedule ? o.schedule : 1;
     p->D = D;
     p->nchunks = (N + 64 * K - 1) / (64 * K);
   } else {
@@ -169,6 +172,8 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, in
     p->D = 64 * G;
     p->nchunks = (N + NB - 1) / NB;
   }
+  if (kernel != 3 && o.schedule == 2)
+    return fail(SOM_ERR_INVALID_ARG, "opts->schedule 2 (round-synchronised launches) applies to kernel 3 only");
   p->nunits = (B + p->D - 1) / p->D;
   if (p->nunits >= kMaxTiles)
     return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: too many tiles or groups");
@@ -290,6 +295,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
   a.nchunks = p.nchunks;
   a.tile_base = 0;
   a.tile_end = p.nunits;
+  a.schedule = p.schedule;
   if (p.kernel == 1 || p.kernel == 3) {
     a.tile_offset = at<int32_t>(plan, l.offset);
     a.tile_count = at<int32_t>(plan, l.count);
@@ -320,7 +326,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 12; }
+int32_t som_abi_version(void) { return 13; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 

@@ -82,6 +82,14 @@ struct SearchArgs {
   int64_t nchunks;  // neuron slices = ceil(N / (64 * K))
   int64_t tile_base = 0;  // kernel 1 searches tiles [tile_base, tile_end) of the plan
   int64_t tile_end = 0;
+  // kernel 3, round-synchronised launches (round_wgs > 0): one launch per
+  // (neuron slice, round); XCD x searches super-tiles x * xcd_span +
+  // round_base + [0, round_wgs) of slice slice_base
+  int32_t schedule = 0;   // 1 = one launch over every slice, 2 = rounds
+  int32_t round_wgs = 0;
+  int64_t round_base = 0;
+  int64_t xcd_span = 0;
+  int64_t slice_base = 0;
   float* score = nullptr;  // unfused comparator: distances of tiled-order documents
                            // [tile_base * T, ...) go to score[(p - tile_base * T) * N + j]
   const int32_t* tile_offset;

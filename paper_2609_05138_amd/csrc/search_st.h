@@ -110,9 +110,22 @@ k_search_st(SearchArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   // XCD-contiguous super-tile ranges (see k_search)
-  const uint32_t per_xcd = gridDim.x / kXcds;
-  const int64_t st = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  const int64_t c = blockIdx.y;
+  int64_t st, c;
+  if (a.round_wgs) {
+    // one round of one slice: every workgroup of the launch is resident at
+    // once, so the round's super-tiles start together and sweep their
+    // ascending unions side by side (each XCD's L2 holds the rows of the
+    // feature range they share); XCD x takes the next round_wgs super-tiles
+    // of its own contiguous range
+    const int64_t j = blockIdx.x / kXcds;
+    if (a.round_base + j >= a.xcd_span) return;
+    st = (blockIdx.x % kXcds) * a.xcd_span + a.round_base + j;
+    c = a.slice_base;
+  } else {
+    const uint32_t per_xcd = gridDim.x / kXcds;
+    st = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    c = blockIdx.y;
+  }
   if (st >= a.ntiles) return;  // whole workgroup: no barrier is skipped by part of it
 
   const int64_t n0 = c * WN;
@@ -291,6 +304,37 @@ hipError_t launch_st(const SearchArgs& a, hipStream_t stream) {
   // stages, deeper rings and 16-document waves were slower.
   constexpr int P = 16;
   constexpr int NSLOT = 2;
+  if (a.schedule == 2) {
+    // round-synchronised launches: per slice, rounds of R super-tiles per
+    // XCD, R = the workgroups one XCD holds at once (its CUs times the
+    // kernel's occupancy per CU), so a launch's workgroups all start together
+    const void* fn = a.mask_mode == 2 ? reinterpret_cast<const void*>(k_search_st<WT, T, K, S, P, NSLOT, kStDocMajor>)
+                                      : reinterpret_cast<const void*>(k_search_st<WT, T, K, S, P, NSLOT, kStRowMajor>);
+    int per_cu = 0, dev = 0, cus = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, S * 64, 0);
+    if (e != hipSuccess) return e;
+    e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const int R = per_cu * cus / static_cast<int>(kXcds) > 0 ? per_cu * cus / static_cast<int>(kXcds) : 1;
+    SearchArgs b = a;
+    b.round_wgs = R;
+    b.xcd_span = (a.ntiles + kXcds - 1) / kXcds;
+    const int64_t rounds = (b.xcd_span + R - 1) / R;
+    const dim3 grid(static_cast<uint32_t>(kXcds * R), 1);
+    for (int64_t c = 0; c < a.nchunks; ++c) {
+      b.slice_base = c;
+      for (int64_t r = 0; r < rounds; ++r) {
+        b.round_base = r * R;
+        if (a.mask_mode == 2)
+          hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT, kStDocMajor>), grid, dim3(S * 64), 0, stream, b);
+        else
+          hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT, kStRowMajor>), grid, dim3(S * 64), 0, stream, b);
+      }
+    }
+    return hipGetLastError();
+  }
   const dim3 grid(static_cast<uint32_t>((a.ntiles + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));
   if (a.mask_mode == 2)
     hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT, kStDocMajor>), grid, dim3(S * 64), 0, stream, a);

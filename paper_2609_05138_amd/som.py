@@ -71,6 +71,7 @@ class som_bmu_opts(ctypes.Structure):
         ("slice_neurons", ctypes.c_int32),
         ("validate", ctypes.c_int32),
         ("storage", ctypes.c_int32),
+        ("schedule", ctypes.c_int32),
     ]
 
 
@@ -191,9 +192,9 @@ def _stream(stream) -> ctypes.c_void_p:
 
 
 def _opts(kernel=0, tile_docs=0, lane_neurons=0, group_tiles=0, mask_mode=0, slice_neurons=0,
-          validate=False, storage=0) -> som_bmu_opts:
+          validate=False, storage=0, schedule=0) -> som_bmu_opts:
     return som_bmu_opts(int(kernel), int(tile_docs), int(lane_neurons), int(group_tiles), int(mask_mode),
-                        int(slice_neurons), int(bool(validate)), int(storage))
+                        int(slice_neurons), int(bool(validate)), int(storage), int(schedule))
 
 
 def _n_neurons(N, norms, W) -> int:

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 12
+    assert som.som_abi_version() == 13
 
 
 def test_automatic_launch_follows_the_storage_type(lib):
@@ -167,7 +167,8 @@ def test_search_rejects_bad_arguments(lib):
     for bad in (O(4), O(-1), O(3, 32), O(3, 16), O(3, 0, 8), O(3, 0, 0, 2), O(3, 0, 0, 0, 3), O(3, 0, 0, 0, 0, 32),
                 O(1, 5), O(1, 0, 3), res, O(1, 0, 0, 16), O(1, 0, 0, 0, 3), O(1, 32, 8),
                 O(0, 0, 0, 0, 0, 0, 2), O(1, 0, 0, -1), O(2, 8), O(2, 0, 4), O(2, 0, 0, 1),
-                O(2, 0, 0, 0, 1), O(2, 0, 0, 0, 0, 48), O(1, 0, 0, 0, 0, 32)):
+                O(2, 0, 0, 0, 1), O(2, 0, 0, 0, 0, 48), O(1, 0, 0, 0, 0, 32),
+                O(0, 0, 0, 0, 0, 0, 0, 0, 3), O(1, 0, 0, 0, 0, 0, 0, 0, 2), O(3, 0, 0, 0, 0, 0, 0, 0, -1)):
         st, msg = call(opts=ctypes.byref(bad))
         assert st == som.SOM_ERR_INVALID_ARG, msg
     # an empty batch is a valid no-op that touches nothing

@@ -144,7 +144,8 @@ def test_dyadic_codebook_bit_exact_with_ties(N):
     for knobs in (dict(kernel=1, tile_docs=1), dict(kernel=1, tile_docs=8), dict(kernel=1, tile_docs=32),
                   dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64),
                   dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256),
-                  dict(kernel=3, mask_mode=2), dict(kernel=3, tile_docs=256, mask_mode=2)):
+                  dict(kernel=3, mask_mode=2), dict(kernel=3, tile_docs=256, mask_mode=2),
+                  dict(kernel=3, schedule=2), dict(kernel=3, tile_docs=128, mask_mode=1, schedule=2)):
         bmu, dist, _ = _search(W, indptr, indices, **knobs)
         assert bmu.tolist() == [e[2][0] for e in exact]
         assert [Fraction(float(x)) for x in dist] == [Fraction(e[1], 16) for e in exact]

@@ -33,7 +33,7 @@ KNOBS = [dict(kernel=1, tile_docs=T) for T in (1, 4, 8, 16, 32)] + [
     dict(kernel=1, lane_neurons=8), dict(kernel=1, group_tiles=4, mask_mode=1),
     dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64),
     dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256),
-    dict(kernel=3, mask_mode=2), dict(kernel=3, tile_docs=256, mask_mode=2)]
+    dict(kernel=3, mask_mode=2), dict(kernel=3, tile_docs=256, mask_mode=2), dict(kernel=3, schedule=2)]
 
 
 def _csr(docs):
