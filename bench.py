@@ -52,7 +52,19 @@ REL = 1e-5
 # read for a plain 4 GiB device copy (x2.0 and x1.0).  Each entry holds the
 # digest of the kernel sources it was measured on: after any change to them
 # the entry no longer matches and `traffic` is reported as null.
-MEASURED_TRAFFIC = {}
+MEASURED_TRAFFIC = {
+    # the default run: the 2,000,000-document 512^2 pass, kernel 3 (automatic)
+    json.dumps(["map512x512-F20000-2M", [0, 1], 0, 262208, "f32", False, False, False, False,
+                {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "schedule": 0,
+                 "slice_neurons": 0, "storage": 0, "tile_docs": 0}]): {
+        "csrc": "6934b1ca762e3b97",
+        "fetch_kib": [9.1602e9, 8.3397e9],       # per search launch (batch 0, batch 1)
+        "write_kib": [3.3554e7, 3.0446e7],
+        "fetch_scale": 2.0, "write_scale": 1.0,   # plain 4 GiB device copy: FETCH_SIZE reads half, WRITE_SIZE exact
+        "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,1>, "
+                  "profiles/search_st_map512_2M_counters.md",
+    },
+}
 
 
 def csrc_digest() -> str:

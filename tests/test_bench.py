@@ -65,6 +65,12 @@ def test_counter_entries_belong_to_the_current_kernels():
     for key, entry in bench.MEASURED_TRAFFIC.items():
         assert entry["csrc"] == digest, (key, "kernel sources changed since these counters were taken")
         assert len(entry["fetch_kib"]) == len(entry["write_kib"]) == len(json.loads(key)[1])
+    # the default run (the whole 512^2 pass, automatic launch) has its counters
+    from synth import CONFIGS
+    knobs = bench.launch_knobs(bench.parse([]), CONFIGS[4])
+    key = json.dumps([CONFIGS[4].name, [0, 1], 0, 262208, "f32", False, False, False, False,
+                      {k: v for k, v in sorted(knobs.items())}])
+    assert key in bench.MEASURED_TRAFFIC
 
 
 def test_oracle_sample_plan():
