@@ -511,13 +511,17 @@ def main():
     probes = None
     if not args.no_probe:
         sink = torch.empty(1, dtype=torch.int32, device=dev)
-        wbytes_all = Wd.numel() * Wd.element_size()
+        # the codebook itself when it is large (the HBM figure is one pass over
+        # it), else a 2 GiB buffer of its own (small maps)
+        pbuf = Wd if Wd.numel() * Wd.element_size() >= (2 << 30) else torch.zeros(2 << 30, dtype=torch.uint8,
+                                                                                   device=dev)
+        wbytes_all = pbuf.numel() * pbuf.element_size()
 
         def rate(nbytes, passes):
-            som.som_probe_read(Wd, nbytes, 1, sink)           # first touch (fills the caches)
+            som.som_probe_read(pbuf, nbytes, 1, sink)         # first touch (fills the caches)
             e0, e1 = ev(), ev()
             e0.record(stream)
-            som.som_probe_read(Wd, nbytes, passes, sink)
+            som.som_probe_read(pbuf, nbytes, passes, sink)
             e1.record(stream)
             torch.cuda.synchronize()
             return nbytes * passes / (e0.elapsed_time(e1) * 1e-3)

@@ -278,8 +278,16 @@ __device__ __forceinline__ void epilogue(const SearchArgs& a, const float (&acc)
   }
 }
 
+// Waves per SIMD the register budget must allow: 16-document fp32 tiles fit
+// five (at most 96 VGPRs), which the memory-latency-bound loop needs; the
+// register allocator is otherwise free to settle just above that line.
+template <typename WT, int T, int K>
+constexpr int k1_min_waves() {
+  return (sizeof(WT) == 4 && T == 16 && K == 4) ? 5 : 1;
+}
+
 template <typename WT, int T, int K, int G, int U, int MODE>
-__global__ void __launch_bounds__(G * 64)
+__global__ void __launch_bounds__(G * 64) __attribute__((amdgpu_waves_per_eu(k1_min_waves<WT, T, K>())))
 k_search(SearchArgs a) {
   constexpr int E = Storage<WT>::kE;  // elements per 128-bit load
   constexpr int Q = K / E;            // loads per lane per row
@@ -314,12 +322,15 @@ k_search(SearchArgs a) {
   // accumulators E*q .. E*q + E - 1.  Byte offsets inside a row slice; lanes
   // past the last neuron re-read the last group holding one (never reported),
   // so no load leaves [0, round_up(N, E)) of its row.
+  // The limit is slice-relative and wave-uniform: 32-bit scalar arithmetic
+  // keeps the per-lane cost to one compare and select.
   const int64_t nv = (a.N + E - 1) / E * E;
+  const int32_t lim = static_cast<int32_t>(nv - n0 < WN ? nv - n0 : WN);  // valid columns of the slice
   uint32_t offb[Q];
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
-    const int64_t o = 64 * E * q + E * lane;
-    offb[q] = static_cast<uint32_t>(sizeof(WT) * (n0 + o < nv ? o : nv - E - n0));
+    const int32_t o = 64 * E * q + E * lane;
+    offb[q] = static_cast<uint32_t>(sizeof(WT)) * static_cast<uint32_t>(o < lim ? o : lim - E);
   }
   const int32_t u0 = a.tile_offset[t];
   const int32_t cnt = a.tile_count[t];
