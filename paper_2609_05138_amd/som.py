@@ -14,7 +14,9 @@ from typing import Optional, Tuple
 import torch  # imported before the library so both share one HIP runtime
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libsom.so")
+# SOM_LIBRARY names another build of the same library (the host-sanitized
+# one, for CPU-side checks); it must exist like the default one
+LIB_PATH = os.environ.get("SOM_LIBRARY") or os.path.join(_PKG, "libsom.so")
 
 SOM_OK = 0
 SOM_ERR_INVALID_ARG = 1
