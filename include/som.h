@@ -96,9 +96,11 @@ typedef struct som_bmu_opts {
   int32_t group_tiles;   /* kernel 1: tiles per workgroup, 0 (auto: see above), 1, 2, 4 or 8;
                             kernel 2: waves per workgroup G, 0 (auto), 4, 8 or 16 */
   int32_t mask_mode;     /* kernel 1: 0 = auto, 1 = branch-free multiply by the membership
-                            bit, 2 = one scalar branch per document; kernel 3: 0 = auto (1),
-                            1 = one visit per needed row with a scalar branch tree over the
-                            wave's documents, 2 = one ballot per document over each stage */
+                            bit, 2 = one scalar branch per document; kernel 3: 0 = auto (2),
+                            1 = row-major: one visit per row the wave needs, with a scalar
+                            branch tree over the wave's documents, 2 = document-major: per
+                            document, the stage entries it holds, read from the plan's
+                            per-stage document words */
   int32_t slice_neurons; /* kernel 2: NB = 0 (auto), 32 or 64 */
   int32_t validate;      /* 1 = check the CSR batch on the device first (synchronises `stream`) */
   int32_t storage;       /* 0 = fp32, 1 = fp16: the codebook storage type whose automatic tile

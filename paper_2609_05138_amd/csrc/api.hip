@@ -195,7 +195,8 @@ size_t take(size_t& o, size_t bytes) {
 
 // Plan layout (each region 256-byte aligned): offsets [nunits+1], counts
 // [nunits], union features [nnz], then kernel 1 masks or kernel 2 entry
-// positions [nnz]; kernel 3: features [nnz + 256], masks [nnz + 256][D / 32].
+// positions [nnz]; kernel 3: features [nnz + pad], masks [nnz + pad][D / 32],
+// pad = 256 entries, plus 16 per tile with stage masks.
 struct PlanLayout {
   size_t offset, count, feat, extra, total;
 };

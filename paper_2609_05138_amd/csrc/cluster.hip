@@ -109,7 +109,7 @@ int key_bits(int64_t F) {
 // descending otherwise; k runs over 2, 4, .., n2 and, for each k, j over
 // k/2, k/4, .., 1.  Steps with j < kLocal stay inside aligned blocks of
 // kLocal elements and run in LDS (one launch for a run of them); wider
-// steps run one launch each over global memory.
+// steps run over global memory, up to three of them per launch.
 // ---------------------------------------------------------------------------
 constexpr int kLocal = 2048;           // elements per LDS block
 constexpr int kLocalThreads = kLocal / 2;
@@ -175,6 +175,50 @@ k_bitonic_global(uint64_t* __restrict__ keys, uint32_t* __restrict__ vals, int64
   }
 }
 
+// Steps (k, j), (k, j/2), .., (k, j/2^(L-1)) in one launch, all with
+// j/2^(L-1) >= kLocal: thread t holds the R = 2^L elements base + m*q
+// (q = j/2^(L-1), m = 0 .. R-1; base is t with L clear bits inserted at q),
+// which those steps pair only among themselves, in registers.  The elements
+// span 2j <= k, so they share bit k and one direction.
+template <int L>
+__global__ void __launch_bounds__(256)
+k_bitonic_global_multi(uint64_t* __restrict__ keys, uint32_t* __restrict__ vals, int64_t n2, int64_t k, int64_t j) {
+  constexpr int R = 1 << L;
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= n2 / R) return;
+  const int64_t q = j >> (L - 1);
+  const int64_t base = ((t & ~(q - 1)) << L) | (t & (q - 1));
+  const bool asc = (base & k) == 0;
+  uint64_t kk[R];
+  uint32_t vv[R];
+#pragma unroll
+  for (int m = 0; m < R; ++m) {
+    kk[m] = keys[base + m * q];
+    vv[m] = vals[base + m * q];
+  }
+#pragma unroll
+  for (int s = L - 1; s >= 0; --s) {
+#pragma unroll
+    for (int m = 0; m < R; ++m) {
+      const int d = 1 << s;
+      if (m & d) continue;
+      if (pair_greater(kk[m], vv[m], kk[m + d], vv[m + d]) == asc) {
+        const uint64_t tk = kk[m];
+        const uint32_t tv = vv[m];
+        kk[m] = kk[m + d];
+        vv[m] = vv[m + d];
+        kk[m + d] = tk;
+        vv[m + d] = tv;
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < R; ++m) {
+    keys[base + m * q] = kk[m];
+    vals[base + m * q] = vv[m];
+  }
+}
+
 __global__ void __launch_bounds__(256)
 k_perm_out(const uint32_t* __restrict__ vals, int64_t B, int32_t* __restrict__ perm) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -211,9 +255,23 @@ hipError_t launch_cluster(const int32_t* indptr, const int32_t* indices, int64_t
     hipLaunchKernelGGL(k_bitonic_local, dim3(nblk), dim3(static_cast<uint32_t>(blk / 2)), 0, stream, keys, vals,
                        blk, int64_t(2), blk, int64_t(1));
     for (int64_t k = 2 * blk; k <= n2; k <<= 1) {
-      for (int64_t j = k >> 1; j >= blk; j >>= 1)
-        hipLaunchKernelGGL(k_bitonic_global, dim3(static_cast<uint32_t>((n2 / 2 + 255) / 256)), dim3(256), 0,
-                           stream, keys, vals, n2, k, j);
+      // the wide steps three (or two) at a time, the last odd one alone
+      int64_t j = k >> 1;
+      while (j >= blk) {
+        if (j >= 4 * blk) {
+          hipLaunchKernelGGL(k_bitonic_global_multi<3>, dim3(static_cast<uint32_t>((n2 / 8 + 255) / 256)), dim3(256),
+                             0, stream, keys, vals, n2, k, j);
+          j >>= 3;
+        } else if (j >= 2 * blk) {
+          hipLaunchKernelGGL(k_bitonic_global_multi<2>, dim3(static_cast<uint32_t>((n2 / 4 + 255) / 256)), dim3(256),
+                             0, stream, keys, vals, n2, k, j);
+          j >>= 2;
+        } else {
+          hipLaunchKernelGGL(k_bitonic_global, dim3(static_cast<uint32_t>((n2 / 2 + 255) / 256)), dim3(256), 0,
+                             stream, keys, vals, n2, k, j);
+          j >>= 1;
+        }
+      }
       hipLaunchKernelGGL(k_bitonic_local, dim3(nblk), dim3(static_cast<uint32_t>(blk / 2)), 0, stream, keys, vals,
                          blk, k, k, blk >> 1);
     }

@@ -24,10 +24,13 @@
 // then one barrier makes every wave's part visible and closes stage s-1,
 // whose slot the loads of stage s+NSLOT-1 then reuse.  The feature ids of
 // those loads arrive with stage s itself (spare lanes of its mask load).  Entries past the
-// union's end load row 0 and get empty masks.  A wave skips the entries of a
-// stage its documents do not hold: a ballot over the stage's masks (lane r
-// holds entry r's word) gives the needed entries, visited in ascending order
-// with the next row's LDS read issued before the current row's adds.
+// union's end load row 0 and get empty masks.  A wave adds only the entries
+// of a stage its documents hold, in one of two dispatch forms (StDispatch
+// below): row-major (a ballot over the stage's entry masks gives the needed
+// rows, visited in ascending order with the next row's LDS read issued
+// before the current row's adds) or document-major (the default: per
+// document, the stage entries it holds, from 16-bit document words that the
+// plan stores per stage and the wave reads with scalar loads a stage ahead).
 //
 // Included by the translation units that instantiate it; internal linkage.
 #pragma once
