@@ -159,8 +159,13 @@ k_search_st(SearchArgs a) {
   // Each stage's dword load carries, per lane: lanes r < P the wave's mask
   // word of entry r of the stage; lanes P + r the feature id of entry r of the
   // stage NSLOT-1 later (so the row loads issued after a stage's barrier need
-  // no scalar load); other lanes repeat lane r & (P-1)'s word.
+  // no scalar load); other lanes repeat lane r & (P-1)'s word.  With the
+  // document-major dispatch (masks from the plan's stage words) only the id
+  // lanes of the wave's own rows load: fewer addresses for the texture
+  // addresser per stage (1.5% faster at 512^2; scalar loads of those ids a
+  // stage ahead, in place of the dword load, were 3% slower).
   const bool id_lane = lane >= P && lane < 2 * P;
+  const bool id_mine = lane >= P + wave * RPW && lane < P + wave * RPW + RPW;
   const uint32_t* __restrict__ dsrc =
       id_lane ? reinterpret_cast<const uint32_t*>(a.union_feat + u0 + (NSLOT - 1) * P + (lane - P))
               : a.union_mask + (static_cast<int64_t>(u0) + (lane & (P - 1))) * MW + mword;
@@ -193,7 +198,7 @@ k_search_st(SearchArgs a) {
       const int64_t f = e < cnt ? (fid)[i] : 0;                                               \
       dma_b128(Wn + f * ldw_b, ring0 + slot_ * (P * 1024) + static_cast<uint32_t>(i * 1024)); \
     }                                                                                         \
-    dma_b32(dsrc + q_ * dstride, mring0 + slot_ * (S * 256));                                 \
+    if (DISP != kStDocMajor || id_mine) dma_b32(dsrc + q_ * dstride, mring0 + slot_ * (S * 256)); \
   }
 #pragma unroll
     for (int q = 0; q < NSLOT - 1; ++q) {
@@ -228,7 +233,7 @@ k_search_st(SearchArgs a) {
                                static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), src));
             dma_b128(Wn + o, ring0 + slot_ * (P * 1024) + static_cast<uint32_t>(i * 1024));
           }
-          dma_b32(dsrc + q * dstride, mring0 + slot_ * (S * 256));
+          if (id_mine) dma_b32(dsrc + q * dstride, mring0 + slot_ * (S * 256));
         } else {
           int32_t fid[RPW];
 #pragma unroll
