@@ -226,7 +226,10 @@ def test_cluster_order_golden():
         assert perm.tolist() == ex["perm"]
 
 
-@pytest.mark.parametrize("cfg,n", [(5, 20000), (2, 8000), (1, 10000)])
+# sizes reach every launch form of the sort: steps inside 2,048-element
+# blocks only, and one, two or three wide steps per launch (n2 = 2^18 runs
+# seven merge levels above the block size)
+@pytest.mark.parametrize("cfg,n", [(5, 20000), (2, 8000), (1, 10000), (2, 150000)])
 def test_cluster_order_bit_exact(cfg, n):
     from synth import CONFIGS, documents
     indptr, indices = documents(cfg, 0, n_docs=n)
