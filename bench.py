@@ -55,10 +55,10 @@ REL = 1e-5
 MEASURED_TRAFFIC = {
     # the default run: the 2,000,000-document 512^2 pass, kernel 3 (automatic)
     json.dumps(["map512x512-F20000-2M", [0, 1], 0, 262208, "f32", False, False, False, False,
-                {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "schedule": 0,
-                 "slice_neurons": 0, "storage": 0, "tile_docs": 0}]): {
-        "csrc": "885a6c7af7cde006",
-        "fetch_kib": [9.0875e9, 8.3362e9],       # per search launch (batch 0, batch 1)
+                {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
+                 "schedule": 0, "slice_neurons": 0, "storage": 0, "tile_docs": 0}]): {
+        "csrc": "0005255242b284f8",
+        "fetch_kib": [9.1092e9, 8.3034e9],       # per search launch (batch 0, batch 1)
         "write_kib": [3.3554e7, 3.0446e7],
         "fetch_scale": 2.0, "write_scale": 1.0,   # plain 4 GiB device copy: FETCH_SIZE reads half, WRITE_SIZE exact
         "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,1>, "
@@ -66,10 +66,10 @@ MEASURED_TRAFFIC = {
     },
     # batch 0 of the topic pass (--config 5 --batch 0), kernel 3 (automatic)
     json.dumps(["map512x512-F20000-26.9M-topics", [0], 0, 262208, "f32", False, False, False, False,
-                {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "schedule": 0,
-                 "slice_neurons": 0, "storage": 0, "tile_docs": 0}]): {
-        "csrc": "885a6c7af7cde006",
-        "fetch_kib": [1.8695e10],
+                {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
+                 "schedule": 0, "slice_neurons": 0, "storage": 0, "tile_docs": 0}]): {
+        "csrc": "0005255242b284f8",
+        "fetch_kib": [1.8692e10],
         "write_kib": [3.2000e7],
         "fetch_scale": 2.0, "write_scale": 1.0,
         "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,1>, "
@@ -109,6 +109,8 @@ def parse(argv=None):
     p.add_argument("--slice-neurons", type=int, default=0)
     p.add_argument("--schedule", type=int, default=0,
                    help="kernel 3: 0 = auto, 1 = one launch, 2 = round-synchronised launches")
+    p.add_argument("--neuron-chunk", type=int, default=0,
+                   help="kernels 1 and 3: neurons per schedule chunk (0 = one slice)")
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage (input order)")
     p.add_argument("--stream", action="store_true",
                    help="batches in pinned host memory, uploaded and planned on a side stream")
@@ -145,7 +147,8 @@ def launch_knobs(args, cfg):
     kernel = args.kernel or (1 if args.unfused else 0)
     return dict(kernel=kernel, tile_docs=args.tile_docs, lane_neurons=args.lane_neurons,
                 group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons,
-                storage=1 if args.weights == "f16" else 0, schedule=args.schedule)
+                storage=1 if args.weights == "f16" else 0, schedule=args.schedule,
+                neuron_chunk=args.neuron_chunk)
 
 
 def sample_docs(sizes, cfg_key, batches, total, seed=2024):

@@ -110,6 +110,12 @@ typedef struct som_bmu_opts {
                             2 = round-synchronised launches: per slice, one launch per round of
                             as many super-tiles as the device holds at once, so that they sweep
                             their ascending unions side by side; kernels 1 and 2: 0 or 1 */
+  int32_t neuron_chunk;  /* kernels 1 and 3 (schedule 1): neurons per schedule chunk (Section 4.2,
+                            "Neuron-axis chunking"), 0 = auto (one slice, 64 * K neurons) or a
+                            multiple of the slice width.  The launch visits the neuron axis chunk
+                            by chunk; inside a chunk each XCD takes its tiles in turn and runs a
+                            tile's slices of the chunk back to back.  Chunks wider than the map
+                            cover it whole. */
 } som_bmu_opts;
 
 /* Version of this ABI (bumped on any incompatible change). */

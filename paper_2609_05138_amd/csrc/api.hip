@@ -82,6 +82,7 @@ struct Plan {
   int64_t nchunks = 0;  // neuron slices
   bool stage_masks = false;  // kernel 3, document-major: masks stored per stage and document
   int schedule = 1;          // 1 = one launch, 2 = round-synchronised launches (kernel 3)
+  int chunk_slices = 1;      // kernels 1 and 3: neuron slices per schedule chunk
 };
 
 // Kernel-1 tiles per workgroup chosen automatically: four consecutive tiles
@@ -174,6 +175,16 @@ som_status make_plan(int64_t N, int64_t B, const som_bmu_opts* opts, Plan* p, in
   }
   if (kernel != 3 && o.schedule == 2)
     return fail(SOM_ERR_INVALID_ARG, "opts->schedule 2 (round-synchronised launches) applies to kernel 3 only");
+  if (o.neuron_chunk < 0) return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk must be >= 0");
+  if (o.neuron_chunk) {
+    const int64_t width = 64 * static_cast<int64_t>(p->K);
+    if (kernel == 2) return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk applies to kernels 1 and 3 only");
+    if (p->schedule == 2) return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk needs schedule 1 (one launch)");
+    if (o.neuron_chunk % width)
+      return fail(SOM_ERR_INVALID_ARG, "opts->neuron_chunk must be a multiple of the slice width (64 * K neurons)");
+    const int64_t q = o.neuron_chunk / width;
+    p->chunk_slices = static_cast<int>(q < p->nchunks ? q : (p->nchunks > 0 ? p->nchunks : 1));
+  }
   p->nunits = (B + p->D - 1) / p->D;
   if (p->nunits >= kMaxTiles)
     return fail(SOM_ERR_INVALID_ARG, "batch too large for one launch: too many tiles or groups");
@@ -291,6 +302,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
   a.K = p.K;
   a.group = p.group;
   a.mask_mode = p.mask_mode;
+  a.chunk_slices = p.chunk_slices;
   a.slice = p.NB;
   a.ntiles = p.nunits;
   a.nchunks = p.nchunks;
@@ -327,7 +339,7 @@ som_status run_planned(const void* W, int weights, int64_t F, int64_t N, int64_t
 
 extern "C" {
 
-int32_t som_abi_version(void) { return 13; }
+int32_t som_abi_version(void) { return 14; }
 
 const char* som_last_error(void) { return g_error.c_str(); }
 
@@ -779,6 +791,7 @@ som_status som_bmu_search_unfused(const float* W, int64_t F, int64_t N, int64_t 
   a.K = p.K;
   a.group = p.group;
   a.mask_mode = p.mask_mode;
+  a.chunk_slices = p.chunk_slices;
   a.ntiles = p.nunits;
   a.nchunks = p.nchunks;
   a.tile_offset = at<int32_t>(ws, w.plan.offset);

@@ -65,6 +65,23 @@ hipError_t launch_group_plan(const int32_t* indptr, const int32_t* indices, int6
                              const int32_t* perm, int D, int32_t* group_offset, int32_t* group_count,
                              int32_t* group_feat, int32_t* entry_pos, hipStream_t stream);
 
+// Block index -> (tile or tile-group index, neuron slice) of a kernel-1/3
+// launch over a grid of nx (a multiple of 8) x nslices workgroups, dealt to
+// the XCDs round-robin in linear order.  XCD x owns the contiguous tile range
+// [x * nx/8, (x+1) * nx/8); it visits the neuron slices in chunks of q, and
+// inside a chunk its tiles in turn with the chunk's slices back to back (the
+// last chunk may hold fewer than q slices).  q = 1 is slice-major order.
+__host__ __device__ inline void chunked_block(uint64_t lin, uint64_t nx, uint64_t nslices, uint64_t q,
+                                              uint64_t* unit, uint64_t* slice) {
+  const uint64_t xcd = lin % 8, j = lin / 8, per = nx / 8;
+  const uint64_t full = nslices / q, rest = nslices - full * q;
+  const uint64_t chunk = j / (per * q);
+  const uint64_t r = chunk < full ? j - chunk * per * q : j - full * per * q;
+  const uint64_t qq = chunk < full ? q : rest;
+  *unit = xcd * per + r / qq;
+  *slice = chunk * q + r % qq;
+}
+
 struct SearchArgs {
   const void* W;    // fp32 or fp16 [F][ldw] (see `weights`)
   int weights;      // kWeightsF32 or kWeightsF16 (kernel 1 only)
@@ -90,6 +107,10 @@ struct SearchArgs {
   int64_t round_base = 0;
   int64_t xcd_span = 0;
   int64_t slice_base = 0;
+  // kernels 1 and 3 (one launch over every slice): neuron slices per schedule
+  // chunk; the grid's workgroups walk the chunks in turn, and inside a chunk
+  // each XCD's tiles with their chunk slices back to back (1 = slice-major)
+  int32_t chunk_slices = 1;
   float* score = nullptr;  // unfused comparator: distances of tiled-order documents
                            // [tile_base * T, ...) go to score[(p - tile_base * T) * N + j]
   const int32_t* tile_offset;

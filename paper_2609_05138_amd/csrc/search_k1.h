@@ -303,10 +303,16 @@ k_search(SearchArgs a) {
   // the same residues in every slice row; give each XCD one contiguous range
   // of tile groups instead, so that neighbouring tiles of the (clustered)
   // tiled order, which share features, share that XCD's L2.
-  const uint32_t per_xcd = gridDim.x / kXcds;
-  const uint32_t wg = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  uint64_t wg, c;  // tile group, neuron slice
+  if (a.chunk_slices > 1) {
+    chunked_block(static_cast<uint64_t>(blockIdx.y) * gridDim.x + blockIdx.x, gridDim.x, gridDim.y,
+                  static_cast<uint64_t>(a.chunk_slices), &wg, &c);
+  } else {
+    const uint32_t per_xcd = gridDim.x / kXcds;
+    wg = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    c = blockIdx.y;
+  }
   const int64_t t = a.tile_base + static_cast<int64_t>(wg) * G + wave;  // this wave's tile
-  const int64_t c = blockIdx.y;                                         // neuron slice
   if (t >= a.tile_end) return;                                          // no barriers below
   int2* ent = ent_all[wave];
   if (lane < 2 * U) ent[kEntryChunk + lane] = make_int2(0, 0);

@@ -124,6 +124,12 @@ k_search_st(SearchArgs a) {
     if (a.round_base + j >= a.xcd_span) return;
     st = (blockIdx.x % kXcds) * a.xcd_span + a.round_base + j;
     c = a.slice_base;
+  } else if (a.chunk_slices > 1) {
+    uint64_t u, sl;
+    chunked_block(static_cast<uint64_t>(blockIdx.y) * gridDim.x + blockIdx.x, gridDim.x, gridDim.y,
+                  static_cast<uint64_t>(a.chunk_slices), &u, &sl);
+    st = static_cast<int64_t>(u);
+    c = static_cast<int64_t>(sl);
   } else {
     const uint32_t per_xcd = gridDim.x / kXcds;
     st = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;

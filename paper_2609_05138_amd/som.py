@@ -74,6 +74,7 @@ class som_bmu_opts(ctypes.Structure):
         ("validate", ctypes.c_int32),
         ("storage", ctypes.c_int32),
         ("schedule", ctypes.c_int32),
+        ("neuron_chunk", ctypes.c_int32),
     ]
 
 
@@ -194,9 +195,9 @@ def _stream(stream) -> ctypes.c_void_p:
 
 
 def _opts(kernel=0, tile_docs=0, lane_neurons=0, group_tiles=0, mask_mode=0, slice_neurons=0,
-          validate=False, storage=0, schedule=0) -> som_bmu_opts:
+          validate=False, storage=0, schedule=0, neuron_chunk=0) -> som_bmu_opts:
     return som_bmu_opts(int(kernel), int(tile_docs), int(lane_neurons), int(group_tiles), int(mask_mode),
-                        int(slice_neurons), int(bool(validate)), int(storage), int(schedule))
+                        int(slice_neurons), int(bool(validate)), int(storage), int(schedule), int(neuron_chunk))
 
 
 def _n_neurons(N, norms, W) -> int:

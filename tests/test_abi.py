@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 13
+    assert som.som_abi_version() == 14
 
 
 def test_automatic_launch_follows_the_storage_type(lib):
@@ -168,9 +168,16 @@ def test_search_rejects_bad_arguments(lib):
                 O(1, 5), O(1, 0, 3), res, O(1, 0, 0, 16), O(1, 0, 0, 0, 3), O(1, 32, 8),
                 O(0, 0, 0, 0, 0, 0, 2), O(1, 0, 0, -1), O(2, 8), O(2, 0, 4), O(2, 0, 0, 1),
                 O(2, 0, 0, 0, 1), O(2, 0, 0, 0, 0, 48), O(1, 0, 0, 0, 0, 32),
-                O(0, 0, 0, 0, 0, 0, 0, 0, 3), O(1, 0, 0, 0, 0, 0, 0, 0, 2), O(3, 0, 0, 0, 0, 0, 0, 0, -1)):
+                O(0, 0, 0, 0, 0, 0, 0, 0, 3), O(1, 0, 0, 0, 0, 0, 0, 0, 2), O(3, 0, 0, 0, 0, 0, 0, 0, -1),
+                # neuron_chunk: a multiple of the slice width, kernels 1 and 3, one launch
+                O(1, 0, 0, 0, 0, 0, 0, 0, 0, 100), O(3, 0, 0, 0, 0, 0, 0, 0, 0, -256),
+                O(2, 0, 0, 0, 0, 0, 0, 0, 0, 256), O(3, 0, 0, 0, 0, 0, 0, 0, 2, 256),
+                O(1, 0, 8, 0, 0, 0, 0, 0, 0, 256)):
         st, msg = call(opts=ctypes.byref(bad))
         assert st == som.SOM_ERR_INVALID_ARG, msg
+    # a chunk wider than the map covers it whole
+    assert call(opts=ctypes.byref(O(1, 0, 0, 0, 0, 0, 0, 0, 0, 1 << 20)), ws=fake, B=0, nnz=0, indices=null,
+                bmu=null, dist=null)[0] == som.SOM_OK
     # an empty batch is a valid no-op that touches nothing
     assert call(B=0, nnz=0, indices=null, bmu=null, dist=null, ws=null, ws_bytes=0)[0] == som.SOM_OK
     assert lib.som_last_error().decode() == ""

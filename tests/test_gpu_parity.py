@@ -301,6 +301,13 @@ def test_results_identical_across_tile_chunk_and_order():
         for K, G, mode in ((0, 0, 0), (4, 1, 1), (8 if T < 32 else 4, 8, 2), (4, 2, 2)):
             variants.append(dict(kernel=1, tile_docs=T, lane_neurons=K, group_tiles=G, mask_mode=mode))
     variants += [dict(kernel=3, tile_docs=D, mask_mode=m) for D in SUPER for m in (1, 2)]
+    # schedule chunks of the neuron axis (17 slices of 256 neurons here: full
+    # and partial last chunks, and one chunk wider than the map)
+    variants += [dict(kernel=1, neuron_chunk=nc) for nc in (512, 768, 4096, 1 << 20)]
+    variants += [dict(kernel=1, tile_docs=16, group_tiles=4, neuron_chunk=768),
+                 dict(kernel=1, lane_neurons=8, neuron_chunk=1024)]
+    variants += [dict(kernel=3, neuron_chunk=nc) for nc in (512, 768, 4096)]
+    variants += [dict(kernel=3, tile_docs=128, neuron_chunk=512), dict(kernel=3, mask_mode=1, neuron_chunk=1024)]
     for i, v in enumerate(variants):
         for perm in perms if (i % 5 == 0 or v["kernel"] == 3) else perms[:2]:
             out = _search(W, indptr, indices, perm=perm, **v)
