@@ -56,23 +56,23 @@ MEASURED_TRAFFIC = {
     # the default run: the 2,000,000-document 512^2 pass, kernel 3 (automatic)
     json.dumps(["map512x512-F20000-2M", [0, 1], 0, 262208, "f32", False, False, False, False,
                 {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
-                 "schedule": 0, "slice_neurons": 0, "storage": 0, "tile_docs": 0}]): {
-        "csrc": "0005255242b284f8",
-        "fetch_kib": [9.1092e9, 8.3034e9],       # per search launch (batch 0, batch 1)
+                 "schedule": 0, "slice_neurons": 0, "storage": 0, "sweep": 0, "tile_docs": 0}]): {
+        "csrc": "6175cc992ada7202",
+        "fetch_kib": [5.3552e9, 4.8899e9],       # per search launch (batch 0, batch 1)
         "write_kib": [3.3554e7, 3.0446e7],
         "fetch_scale": 2.0, "write_scale": 1.0,   # plain 4 GiB device copy: FETCH_SIZE reads half, WRITE_SIZE exact
-        "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,1>, "
+        "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,2>, "
                   "profiles/search_st_map512_2M_counters.md",
     },
     # batch 0 of the topic pass (--config 5 --batch 0), kernel 3 (automatic)
     json.dumps(["map512x512-F20000-26.9M-topics", [0], 0, 262208, "f32", False, False, False, False,
                 {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
-                 "schedule": 0, "slice_neurons": 0, "storage": 0, "tile_docs": 0}]): {
-        "csrc": "0005255242b284f8",
-        "fetch_kib": [1.8692e10],
+                 "schedule": 0, "slice_neurons": 0, "storage": 0, "sweep": 0, "tile_docs": 0}]): {
+        "csrc": "6175cc992ada7202",
+        "fetch_kib": [1.3966e10],
         "write_kib": [3.2000e7],
         "fetch_scale": 2.0, "write_scale": 1.0,
-        "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,1>, "
+        "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,2>, "
                   "profiles/search_st_topics_1M_counters.md",
     },
 }
@@ -111,6 +111,8 @@ def parse(argv=None):
                    help="kernel 3: 0 = auto, 1 = one launch, 2 = round-synchronised launches")
     p.add_argument("--neuron-chunk", type=int, default=0,
                    help="kernels 1 and 3: neurons per schedule chunk (0 = one slice)")
+    p.add_argument("--sweep", type=int, default=0,
+                   help="union sweep order: 0 = auto (kernel 3 rotated), 1 = ascending, 2 = rotated")
     p.add_argument("--no-cluster", action="store_true", help="skip the clustering stage (input order)")
     p.add_argument("--stream", action="store_true",
                    help="batches in pinned host memory, uploaded and planned on a side stream")
@@ -148,7 +150,7 @@ def launch_knobs(args, cfg):
     return dict(kernel=kernel, tile_docs=args.tile_docs, lane_neurons=args.lane_neurons,
                 group_tiles=args.group_tiles, mask_mode=args.mask_mode, slice_neurons=args.slice_neurons,
                 storage=1 if args.weights == "f16" else 0, schedule=args.schedule,
-                neuron_chunk=args.neuron_chunk)
+                neuron_chunk=args.neuron_chunk, sweep=args.sweep)
 
 
 def sample_docs(sizes, cfg_key, batches, total, seed=2024):

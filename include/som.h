@@ -53,9 +53,12 @@ typedef enum som_status {
 } som_status;
 
 /* Tuning knobs of the search.  A zero-initialised struct (or NULL) selects
- * the defaults.  None of them changes a result: every document's dot product
- * is summed in ascending feature order whatever the knobs, so outputs are
- * bit-identical across all settings.
+ * the defaults.  Only `sweep` changes a result, and only in rounding: with
+ * the ascending sweep every document's dot product is summed in ascending
+ * feature order whatever the other knobs, so outputs are bit-identical
+ * across all their settings and all kernels; the rotated sweep (kernel 3's
+ * default) sums in a rotated order that is fixed for a given batch, perm,
+ * opts and device.
  *
  * Automatic choices (measured on MI355X at map sizes 32^2 to 512^2, F =
  * 2,048 to 20,000, batches up to 1M documents): for an fp32 codebook kernel
@@ -116,6 +119,20 @@ typedef struct som_bmu_opts {
                             by chunk; inside a chunk each XCD takes its tiles in turn and runs a
                             tile's slices of the chunk back to back.  Chunks wider than the map
                             cover it whole. */
+  int32_t sweep;         /* order of each union sweep: 0 = auto (2 where available, else 1),
+                            1 = ascending feature order, 2 = rotated (kernel 3 with mask_mode 2,
+                            schedule 1 and one-slice chunks only; else SOM_ERR_INVALID_ARG):
+                            each super-tile starts its union at a stage given by its place in
+                            its XCD's share of the launch and wraps round, so that the
+                            super-tiles an XCD runs at once sweep the same feature range
+                            together and share its L2 (measured 19% faster on the topic
+                            workload, neutral on the Zipf maps).  A document's dot product is
+                            then summed in that order, which depends on the plan, the launch's
+                            tile grid and the device's CU count and occupancy, not on the
+                            codebook or the neuron range: results are reproducible on one
+                            device type and column ranges compose exactly, but may differ from
+                            the ascending sweep's in the last bits of dist (and, at exact or
+                            near ties, in bmu). */
 } som_bmu_opts;
 
 /* Version of this ABI (bumped on any incompatible change). */
@@ -163,7 +180,7 @@ size_t som_bmu_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,
  *           input order.
  *   bmu     int32 [B] output: argmin_j d_j (lowest index on exact ties)
  *   dist    fp32 [B] output: d_bmu, the squared distance |S| + ||w||^2 - 2 dot
- *           evaluated in fp32 (dot summed in ascending feature order)
+ *           evaluated in fp32 (dot summed in the order opts->sweep names)
  *   ws      device workspace of at least som_bmu_workspace_bytes(...) bytes,
  *           256-byte aligned
  * B == 0 is a valid no-op.  One call is one launch, which takes at most
@@ -314,11 +331,14 @@ som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int6
  * name.  The results are those of the fp32 functions on the codebook whose
  * weights are the fp16 values widened exactly to fp32: norms are the rounded
  * weights' norms (fp64 accumulate, rounded once), and every document's dot
- * product sums the widened weights in ascending feature order, so fp16 and
- * fp32 searches of the same (fp16-representable) codebook are bit-identical.
- * Search knobs: kernel 1 only (kernel 0 or 1), lane_neurons 0 or 8 (a
- * 512-neuron slice, one 128-bit load of 8 weights per lane per row),
- * tile_docs up to 16.  Plans from som_plan are shared with the fp32 search.
+ * product sums the widened weights in the order opts->sweep names, so fp16
+ * and fp32 searches of the same (fp16-representable) codebook are
+ * bit-identical with the ascending sweep (sweep = 1 for the fp32 search,
+ * whose automatic kernel 3 otherwise rotates; the fp16 search's automatic
+ * kernel 1 is ascending).  Search knobs: kernels 1 (the automatic one for
+ * fp16) and 3; lane_neurons 0 or 8 (a 512-neuron slice, one 128-bit load of
+ * 8 weights per lane per row); tile_docs up to 16 for kernel 1, 64 or 128
+ * for kernel 3.  Plans from som_plan are shared with the fp32 search.
  * ------------------------------------------------------------------------- */
 som_status som_codebook_norms_f16(const uint16_t* W, int64_t F, int64_t N, int64_t ldw, float* norms,
                                   hipStream_t stream);
@@ -352,7 +372,8 @@ som_status som_bmu_search_top2_planned_f16(const uint16_t* W, int64_t F, int64_t
  * of block_docs documents at a time (fp32 [block_docs][N], in ws), then one
  * wave per document reduces its row.  The distances are the fused search's
  * fp32 values, so bmu and dist are bit-identical to som_bmu_search's with the
- * same opts.  Kernel 1 (also when opts->kernel is 0) and an fp32 codebook
+ * same opts and the ascending sweep (sweep = 1).  Kernel 1 (also when
+ * opts->kernel is 0; sweep 0 or 1) and an fp32 codebook
  * only; block_docs a positive multiple of the tile size.  ws: som_bmu_search_unfused_workspace_bytes
  * (plan + score block). */
 size_t som_bmu_search_unfused_workspace_bytes(int64_t F, int64_t N, int64_t B, int64_t nnz,

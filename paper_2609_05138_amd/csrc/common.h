@@ -82,6 +82,10 @@ __host__ __device__ inline void chunked_block(uint64_t lin, uint64_t nx, uint64_
   *slice = chunk * q + r % qq;
 }
 
+// Phase period of kernel 3's rotated sweep for super-tiles of S waves of T
+// documents (see search.hip).
+hipError_t st_phase_wgs(int T, int S, int32_t* wgs);
+
 struct SearchArgs {
   const void* W;    // fp32 or fp16 [F][ldw] (see `weights`)
   int weights;      // kWeightsF32 or kWeightsF16 (kernel 1 only)
@@ -111,6 +115,11 @@ struct SearchArgs {
   // chunk; the grid's workgroups walk the chunks in turn, and inside a chunk
   // each XCD's tiles with their chunk slices back to back (1 = slice-major)
   int32_t chunk_slices = 1;
+  // kernel 3, document-major, one launch of one-slice chunks: 1 = rotated
+  // sweep; phase_wgs is its phase period in workgroups per XCD (set by the
+  // launch)
+  int32_t rotate = 0;
+  int32_t phase_wgs = 0;
   float* score = nullptr;  // unfused comparator: distances of tiled-order documents
                            // [tile_base * T, ...) go to score[(p - tile_base * T) * N + j]
   const int32_t* tile_offset;

@@ -268,6 +268,31 @@ hipError_t launch_k1(const SearchArgs& a, hipStream_t stream) {
   }
 }
 
+// Phase period of kernel 3's rotated sweep, in workgroups per XCD: 3/2 of
+// the workgroups one XCD holds at once (its CUs times the occupancy per CU).
+// Measured on the topic workload (1M documents, 512^2 map) over 3/4 to 3
+// times that count, 5/4 to 3/2 were fastest.  It is taken from the fp32
+// kernel of the super-tile's shape for both storage types, so that the fp16
+// and fp32 searches of one plan sum in the same order.
+hipError_t st_phase_wgs(int T, int S, int32_t* wgs) {
+  constexpr int P = 16, NSLOT = 2;
+  const void* fn = nullptr;
+  if (T == 8 && S == 8) fn = reinterpret_cast<const void*>(k_search_st<float, 8, 4, 8, P, NSLOT, kStDocRotated>);
+  if (T == 8 && S == 16) fn = reinterpret_cast<const void*>(k_search_st<float, 8, 4, 16, P, NSLOT, kStDocRotated>);
+  if (T == 16 && S == 16) fn = reinterpret_cast<const void*>(k_search_st<float, 16, 4, 16, P, NSLOT, kStDocRotated>);
+  if (!fn) return hipErrorInvalidValue;
+  int per_cu = 0, dev = 0, cus = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, S * 64, 0);
+  if (e != hipSuccess) return e;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const int M = 3 * per_cu * cus / static_cast<int>(2 * kXcds);
+  *wgs = M > 0 ? M : 1;
+  return hipSuccess;
+}
+
 hipError_t launch_k3(const SearchArgs& a, hipStream_t stream) {
   if (a.weights == kWeightsF16) return launch_search_st_f16(a, stream);
   if (a.K != 4) return hipErrorInvalidValue;

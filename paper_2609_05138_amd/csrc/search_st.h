@@ -32,6 +32,14 @@
 // document, the stage entries it holds, from 16-bit document words that the
 // plan stores per stage and the wave reads with scalar loads a stage ahead).
 //
+// Rotated sweep (the third dispatch form): each super-tile starts its union
+// at a stage chosen from its place in its XCD's work and wraps round, so that
+// the super-tiles an XCD runs at once sweep the same part of the feature
+// range at the same time and share their rows in that XCD's L2 (in ascending
+// order they start at staggered times and spread over the whole range).  A
+// document's dot product is then summed in that rotated order: a fixed order
+// for a given plan and device, different from the ascending one in rounding.
+//
 // Included by the translation units that instantiate it; internal linkage.
 #pragma once
 
@@ -91,8 +99,10 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "me
 //     16-bit word per document: the stage entries it holds); the wave's T
 //     words arrive in scalar registers with one scalar load issued a stage
 //     ahead, and per document each held entry is read from LDS and added,
-//     with a static accumulator index and no per-row scalar branch tree.
-enum StDispatch { kStRowMajor = 0, kStDocMajor = 1 };
+//     with a static accumulator index and no per-row scalar branch tree;
+//   kStDocRotated: kStDocMajor over the stages in rotated order (stage s0 to
+//     the last, then stage 0 to s0 - 1; s0 from the super-tile's phase).
+enum StDispatch { kStRowMajor = 0, kStDocMajor = 1, kStDocRotated = 2 };
 
 template <typename WT, int T, int K, int S, int P, int NSLOT, int DISP>
 __global__ void __launch_bounds__(S * 64)
@@ -102,6 +112,9 @@ k_search_st(SearchArgs a) {
   static_assert(T <= 16 && S * T <= 256, "wave masks fit 16 bits, super-tile masks 8 words");
   static_assert(P <= 32 && P % S == 0 && (P & (P - 1)) == 0, "a stage's masks and ids fit one per lane");
   static_assert(NSLOT * P <= 192, "ids read ahead stay inside the plan's padding");
+  constexpr bool DOC = DISP != kStRowMajor;   // masks from the plan's per-stage document words
+  constexpr bool ROT = DISP == kStDocRotated;
+  static_assert(!ROT || NSLOT == 2, "the rotated sweep tracks the next two stages");
   constexpr int64_t WN = 64 * K;      // neurons per slice
   constexpr int D = S * T;            // documents per super-tile
   constexpr int MW = (D + 31) / 32;   // mask words per union entry
@@ -176,7 +189,35 @@ k_search_st(SearchArgs a) {
       id_lane ? reinterpret_cast<const uint32_t*>(a.union_feat + u0 + (NSLOT - 1) * P + (lane - P))
               : a.union_mask + (static_cast<int64_t>(u0) + (lane & (P - 1))) * MW + mword;
   const int64_t dstride = id_lane ? P : static_cast<int64_t>(P) * MW;  // words per stage
+  // rotated sweep: id lanes load entry lane - P of a stage from here
+  const uint32_t* __restrict__ idl = reinterpret_cast<const uint32_t*>(a.union_feat + u0 + (id_lane ? lane - P : 0));
   const int32_t nstages = (cnt + P - 1) / P;
+  // Rotated sweep: the phase of this super-tile.  An XCD starts its
+  // super-tiles in tile order (one neuron slice after another) with about
+  // a.phase_wgs of them running at once; taking the plan's nonzeros as the
+  // measure of a super-tile's work, one starts when the XCD has done the work
+  // of those before it less the work in flight, so its start time in units
+  // of one super-tile's lifetime is, mod 1, the work of the range's earlier
+  // super-tiles over phase_wgs times the range's mean work per super-tile.
+  // The sweep starts that fraction of the way into the union.  The phase
+  // depends on the plan and the launch's tile grid only (not on the slice),
+  // so column ranges of one codebook still see the same order.
+  int32_t s0 = 0;
+  if (ROT && nstages > 1) {
+    const int64_t per_xcd = gridDim.x / kXcds;
+    const int64_t first = (blockIdx.x % kXcds) * per_xcd;
+    const int64_t end = first + per_xcd < a.ntiles ? first + per_xcd : a.ntiles;
+    const uint64_t o_first = static_cast<uint32_t>(a.tile_offset[first]);
+    const uint64_t work = static_cast<uint32_t>(a.tile_offset[end]) - o_first;  // >= cnt > 0
+    const uint64_t nx = static_cast<uint64_t>(end - first);
+    const uint64_t den = static_cast<uint64_t>(a.phase_wgs) * work;             // < 2^41
+    const uint64_t num = (static_cast<uint32_t>(u0) - o_first) * nx % den;      // product < 2^52
+    const uint64_t ph = (num << 20) / den;                                      // phase in 2^-20
+    s0 = __builtin_amdgcn_readfirstlane(static_cast<int32_t>((ph * static_cast<uint64_t>(nstages)) >> 20));
+  }
+  // stages of sequence steps 1 and 2 (rotated sweep; advanced one per step)
+  int32_t a1 = s0 + 1 >= nstages ? s0 + 1 - nstages : s0 + 1;
+  int32_t a2 = a1 + 1 >= nstages ? a1 + 1 - nstages : a1 + 1;
   // document-major stage masks (P = 16 entries per stage): stage q's word of
   // document j is 16-bit word j at mask word (u0 + q * P) * MW; this wave's
   // T words are T / 2 consecutive 32-bit words
@@ -184,10 +225,10 @@ k_search_st(SearchArgs a) {
   const const_u32 smask = (const_u32)(a.union_mask + static_cast<int64_t>(u0) * MW) + wave * (T / 2);
   constexpr int SW = T / 2;   // 32-bit words of stage masks per wave and stage
   uint32_t dmw[SW];
-  if (DISP == kStDocMajor) {
+  if (DOC) {
     static_assert(P == 16, "document-major stage masks hold 16 entries");
 #pragma unroll
-    for (int k = 0; k < SW; ++k) dmw[k] = nstages > 0 ? smask[k] : 0u;
+    for (int k = 0; k < SW; ++k) dmw[k] = nstages > 0 ? smask[(ROT ? s0 * P * MW : 0) + k] : 0u;
   }
   const uint32_t ring0 = lds_offset(&ring[0][0][0]) + static_cast<uint32_t>(wave * RPW * 1024);
   const uint32_t mring0 = lds_offset(&mring[0][0][0]) + static_cast<uint32_t>(wave * 256);
@@ -200,18 +241,18 @@ k_search_st(SearchArgs a) {
     const int32_t q_ = (q);                                                                   \
     const uint32_t slot_ = static_cast<uint32_t>(q_ % NSLOT);                                 \
     _Pragma("unroll") for (int i = 0; i < RPW; ++i) {                                         \
-      const int32_t e = q_ * P + wave * RPW + i;                                              \
+      const int32_t e = (ROT ? s0 : q_) * P + wave * RPW + i; /* ROT: prologue step 0 only */ \
       const int64_t f = e < cnt ? (fid)[i] : 0;                                               \
       dma_b128(Wn + f * ldw_b, ring0 + slot_ * (P * 1024) + static_cast<uint32_t>(i * 1024)); \
     }                                                                                         \
-    if (DISP != kStDocMajor || id_mine) dma_b32(dsrc + q_ * dstride, mring0 + slot_ * (S * 256)); \
+    if (!DOC || id_mine) dma_b32(ROT ? idl + a1 * P : dsrc + q_ * dstride, mring0 + slot_ * (S * 256)); \
   }
 #pragma unroll
     for (int q = 0; q < NSLOT - 1; ++q) {
       if (q < nstages) {
         int32_t fid[RPW];
 #pragma unroll
-        for (int i = 0; i < RPW; ++i) fid[i] = feat[q * P + wave * RPW + i];
+        for (int i = 0; i < RPW; ++i) fid[i] = feat[(ROT ? s0 : q) * P + wave * RPW + i];
         SOM_ST_ISSUE(q, fid)
       }
     }
@@ -224,11 +265,11 @@ k_search_st(SearchArgs a) {
       const uint32_t w = mring[slot][wave][lane];
       if (s + NSLOT - 1 < nstages) {
         const int32_t q = s + NSLOT - 1;
-        if (DISP == kStDocMajor) {
+        if (DOC) {
           // byte offsets of stage q's rows, computed once on the id lanes
           // (lane P + r holds entry r's feature id; past the union: row 0),
           // then moved to scalar registers one row at a time
-          const bool live = id_lane && q * P + (lane - P) < cnt;
+          const bool live = id_lane && (ROT ? a1 : q) * P + (lane - P) < cnt;
           const uint64_t off = static_cast<uint64_t>(live ? w : 0u) * static_cast<uint64_t>(ldw_b);
           const uint32_t slot_ = static_cast<uint32_t>(q % NSLOT);
 #pragma unroll
@@ -239,7 +280,7 @@ k_search_st(SearchArgs a) {
                                static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), src));
             dma_b128(Wn + o, ring0 + slot_ * (P * 1024) + static_cast<uint32_t>(i * 1024));
           }
-          if (id_mine) dma_b32(dsrc + q * dstride, mring0 + slot_ * (S * 256));
+          if (id_mine) dma_b32(ROT ? idl + a2 * P : dsrc + q * dstride, mring0 + slot_ * (S * 256));
         } else {
           int32_t fid[RPW];
 #pragma unroll
@@ -247,7 +288,7 @@ k_search_st(SearchArgs a) {
           SOM_ST_ISSUE(q, fid)
         }
       }
-      if (DISP == kStDocMajor) {
+      if (DOC) {
         uint32_t cur[SW];
 #pragma unroll
         for (int k = 0; k < SW; ++k) cur[k] = dmw[k];
@@ -273,7 +314,11 @@ k_search_st(SearchArgs a) {
         // stage's first LDS read, after its barrier)
         if (s + 1 < nstages) {
 #pragma unroll
-          for (int k = 0; k < SW; ++k) dmw[k] = smask[(s + 1) * P * MW + k];
+          for (int k = 0; k < SW; ++k) dmw[k] = smask[(ROT ? a1 : s + 1) * P * MW + k];
+        }
+        if (ROT) {
+          a1 = a2;
+          a2 = a2 + 1 >= nstages ? a2 + 1 - nstages : a2 + 1;
         }
         continue;
       }
@@ -350,6 +395,13 @@ hipError_t launch_st(const SearchArgs& a, hipStream_t stream) {
     return hipGetLastError();
   }
   const dim3 grid(static_cast<uint32_t>((a.ntiles + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));
+  if (a.mask_mode == 2 && a.rotate) {
+    SearchArgs b = a;
+    const hipError_t e = st_phase_wgs(T, S, &b.phase_wgs);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT, kStDocRotated>), grid, dim3(S * 64), 0, stream, b);
+    return hipGetLastError();
+  }
   if (a.mask_mode == 2)
     hipLaunchKernelGGL((k_search_st<WT, T, K, S, P, NSLOT, kStDocMajor>), grid, dim3(S * 64), 0, stream, a);
   else

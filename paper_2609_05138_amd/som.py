@@ -75,6 +75,7 @@ class som_bmu_opts(ctypes.Structure):
         ("storage", ctypes.c_int32),
         ("schedule", ctypes.c_int32),
         ("neuron_chunk", ctypes.c_int32),
+        ("sweep", ctypes.c_int32),
     ]
 
 
@@ -195,9 +196,10 @@ def _stream(stream) -> ctypes.c_void_p:
 
 
 def _opts(kernel=0, tile_docs=0, lane_neurons=0, group_tiles=0, mask_mode=0, slice_neurons=0,
-          validate=False, storage=0, schedule=0, neuron_chunk=0) -> som_bmu_opts:
+          validate=False, storage=0, schedule=0, neuron_chunk=0, sweep=0) -> som_bmu_opts:
     return som_bmu_opts(int(kernel), int(tile_docs), int(lane_neurons), int(group_tiles), int(mask_mode),
-                        int(slice_neurons), int(bool(validate)), int(storage), int(schedule), int(neuron_chunk))
+                        int(slice_neurons), int(bool(validate)), int(storage), int(schedule), int(neuron_chunk),
+                        int(sweep))
 
 
 def _n_neurons(N, norms, W) -> int:
@@ -304,8 +306,10 @@ def som_bmu_search(W: torch.Tensor, norms: torch.Tensor, indptr: torch.Tensor, i
     """BMU index (int32) and squared distance (fp32) of every CSR document.
 
     ``N`` defaults to the length of ``norms``.  ``knobs``: kernel, tile_docs,
-    lane_neurons, group_tiles, mask_mode, slice_neurons (fields of
-    som_bmu_opts; none changes a result)."""
+    lane_neurons, group_tiles, mask_mode, slice_neurons, schedule,
+    neuron_chunk, sweep (fields of som_bmu_opts; only sweep changes a
+    result, in rounding: 1 = ascending feature order, 2 = rotated, the
+    kernel-3 default)."""
     return _search(False, W, norms, indptr, indices, N, perm, validate, (bmu, dist), ws, stream, knobs)
 
 

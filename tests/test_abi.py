@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert som.som_abi_version() == 14
+    assert som.som_abi_version() == 15
 
 
 def test_automatic_launch_follows_the_storage_type(lib):
@@ -172,12 +172,26 @@ def test_search_rejects_bad_arguments(lib):
                 # neuron_chunk: a multiple of the slice width, kernels 1 and 3, one launch
                 O(1, 0, 0, 0, 0, 0, 0, 0, 0, 100), O(3, 0, 0, 0, 0, 0, 0, 0, 0, -256),
                 O(2, 0, 0, 0, 0, 0, 0, 0, 0, 256), O(3, 0, 0, 0, 0, 0, 0, 0, 2, 256),
-                O(1, 0, 8, 0, 0, 0, 0, 0, 0, 256)):
+                O(1, 0, 8, 0, 0, 0, 0, 0, 0, 256),
+                # sweep: 0, 1 or 2; the rotated sweep needs kernel 3's document-major single
+                # launch of one-slice chunks
+                O(0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 3), O(3, 0, 0, 0, 0, 0, 0, 0, 0, 0, -1),
+                O(1, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2), O(2, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2),
+                O(3, 0, 0, 0, 1, 0, 0, 0, 0, 0, 2), O(3, 0, 0, 0, 0, 0, 0, 0, 2, 0, 2),
+                O(0, 16, 0, 0, 0, 0, 0, 0, 0, 0, 2)):
         st, msg = call(opts=ctypes.byref(bad))
         assert st == som.SOM_ERR_INVALID_ARG, msg
+    # rotated sweeps with chunks of two slices (the map has four)
+    st, msg = call(opts=ctypes.byref(O(3, 0, 0, 0, 0, 0, 0, 0, 0, 512, 2)), N=1024, ldw=1024)
+    assert st == som.SOM_ERR_INVALID_ARG and "sweep" in msg, msg
     # a chunk wider than the map covers it whole
     assert call(opts=ctypes.byref(O(1, 0, 0, 0, 0, 0, 0, 0, 0, 1 << 20)), ws=fake, B=0, nnz=0, indices=null,
                 bmu=null, dist=null)[0] == som.SOM_OK
+    # the rotated sweep with one-slice chunks, the ascending sweep anywhere
+    for good in (O(0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2), O(3, 128, 0, 0, 2, 0, 0, 0, 1, 256, 2),
+                 O(2, 0, 0, 0, 0, 0, 0, 0, 0, 0, 1), O(3, 0, 0, 0, 1, 0, 0, 0, 2, 0, 1)):
+        assert call(opts=ctypes.byref(good), ws=fake, B=0, nnz=0, indices=null, bmu=null,
+                    dist=null)[0] == som.SOM_OK
     # an empty batch is a valid no-op that touches nothing
     assert call(B=0, nnz=0, indices=null, bmu=null, dist=null, ws=null, ws_bytes=0)[0] == som.SOM_OK
     assert lib.som_last_error().decode() == ""

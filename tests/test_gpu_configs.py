@@ -7,17 +7,18 @@ batch of the pass, each batch's first and last document included; for the
 about 2,048 documents between them (the whole pass, all 27 batches, is
 checked by the benchmark's pass mode).  Each batch is searched in the
 launch configuration the benchmark uses (the library's automatic launch:
-kernel 3 with 64-document super-tiles for an fp32 codebook, kernel 1 with
-8-document tiles for fp16; codebook rows at the recommended stride) and
-checked:
+kernel 3 with 64-document super-tiles and the rotated sweep for an fp32
+codebook, kernel 1 with 8-document tiles for fp16; codebook rows at the
+recommended stride) and checked:
   * sampled documents against the fp64 oracle under the acceptance rule
     (device index equal to the oracle's BMU or inside its 1e-5 near-tie
     band; device distance within 1e-5 relative), the oracle sharded over
     host threads;
   * every document's reported distance against the fp64 distance of the
     reported neuron (a property that holds at any size);
-  * other launch forms on the same batch for bit-identical results, where
-    the benchmark's choice differs from another kernel's.
+  * other launch forms on the same batch for bit-identical results with
+    the ascending sweep (kernel 3 and kernel 1), where the benchmark's
+    choice differs from another kernel's.
 """
 
 import gc
@@ -135,14 +136,16 @@ def _host(*ts):
 
 
 def test_config2_every_document_of_the_first_batch():
-    # 128^2 map, the automatic launch (kernel 3, 64-document super-tiles) on
-    # the clustered order; kernel 1 must give the same bits
+    # 128^2 map, the automatic launch (kernel 3, 64-document super-tiles,
+    # rotated sweep) on the clustered order, every document against the
+    # oracle; with the ascending sweep kernel 3 and kernel 1 give the same bits
     P = _Pass(2)
     indptr, indices, ip, ix = P.batch(0)
     perm = som.som_cluster_order(ip, ix, P.cfg.F)
     bmu, dist = P.search(ip, ix, perm)
     b1, d1 = P.search(ip, ix, perm, kernel=1)
-    assert torch.equal(b1, bmu) and torch.equal(d1, dist), "kernel 1 differs from kernel 3"
+    b3, d3 = P.search(ip, ix, perm, sweep=1)
+    assert torch.equal(b1, b3) and torch.equal(d1, d3), "kernel 1 differs from kernel 3"
     bmu, dist = _host(bmu, dist)
     B = len(indptr) - 1
     bad = _oracle_check(P.W, P.norms64, indptr, indices, np.arange(B), bmu, dist, label="cfg2 batch 0, all")
@@ -160,10 +163,11 @@ def test_config3_sample_over_every_batch():
     for b in range(nb):
         indptr, indices, ip, ix = P.batch(b)
         bmu, dist = P.search(ip, ix, None)
-        if b == nb - 1:   # kernel 1 sums in the same order: the same bits on a whole batch
-            b3, d3 = P.search(ip, ix, None, kernel=1)
-            assert torch.equal(b3, bmu) and torch.equal(d3, dist), "kernel 1 differs from kernel 3"
-            del b3, d3
+        if b == nb - 1:   # ascending sweeps of kernels 1 and 3: the same bits on a whole batch
+            b1, d1 = P.search(ip, ix, None, kernel=1)
+            b3, d3 = P.search(ip, ix, None, sweep=1)
+            assert torch.equal(b3, b1) and torch.equal(d3, d1), "kernel 1 differs from kernel 3"
+            del b1, d1, b3, d3
         bmu, dist = _host(bmu, dist)
         _distance_property(P.W, P.norms64, indptr, indices, bmu.astype(np.int64), dist.astype(np.float64))
         docs = _sample(len(indptr) - 1, SAMPLE // nb, seed=300 + b)
@@ -175,11 +179,12 @@ def test_config3_sample_over_every_batch():
 
 def test_config4_sample_over_both_batches():
     # 512^2 map, 2,000,000 documents in two batches (1,048,576 + 951,424),
-    # clustered, automatic launch (kernel 3): 1,024 sampled documents per
-    # batch.  Batch 0 also checks kernel 1 (16-document tiles, four and one
-    # per workgroup) for identical bits, the top-2 search (same first place,
-    # second place against the oracle) and the fp16 codebook (automatic:
-    # kernel 1, 8-document tiles; kernel 3 for identical bits).
+    # clustered, automatic launch (kernel 3, rotated sweep): 1,024 sampled
+    # documents per batch.  Batch 0 also checks the ascending sweeps of
+    # kernel 3 and kernel 1 (16-document tiles, four and one per workgroup)
+    # for identical bits, the top-2 search (same first place, second place
+    # against the oracle) and the fp16 codebook (automatic: kernel 1,
+    # 8-document tiles; kernel 3 with the ascending sweep for identical bits).
     P = _Pass(4)
     bad = []
     for b in (0, 1):
@@ -190,11 +195,14 @@ def test_config4_sample_over_both_batches():
         second = None
         half = None
         if b == 0:
+            ba, da = P.search(ip, ix, perm, sweep=1)
             b1, d1 = P.search(ip, ix, perm, group_tiles=1)
-            assert torch.equal(b1, bmu) and torch.equal(d1, dist), "kernel 1, one tile per workgroup, differs"
+            assert torch.equal(b1, ba) and torch.equal(d1, da), "kernel 1, one tile per workgroup, differs"
             b3, d3 = P.search(ip, ix, perm, kernel=1)
-            assert torch.equal(b3, bmu) and torch.equal(d3, dist), "kernel 1 differs from kernel 3"
-            del b1, d1, b3, d3
+            assert torch.equal(b3, ba) and torch.equal(d3, da), "kernel 1 differs from kernel 3"
+            flips = int((ba != bmu).sum().item())
+            assert flips <= 50 and not torch.equal(da, dist), flips   # rounding only; the rotation is in effect
+            del ba, da, b1, d1, b3, d3
             t2 = som.som_bmu_search_top2(P.Wd, P.norms, ip, ix, N=P.cfg.N, perm=perm)
             assert torch.equal(t2[0], bmu) and torch.equal(t2[1], dist)
             second = _host(t2[2], t2[3])
@@ -202,7 +210,7 @@ def test_config4_sample_over_both_batches():
             W16d = P.Wd.half()
             n16 = som.som_codebook_norms(W16d, N=P.cfg.N)
             half = _host(*som.som_bmu_search(W16d, n16, ip, ix, N=P.cfg.N, perm=perm))
-            h3 = _host(*som.som_bmu_search(W16d, n16, ip, ix, N=P.cfg.N, perm=perm, kernel=3))
+            h3 = _host(*som.som_bmu_search(W16d, n16, ip, ix, N=P.cfg.N, perm=perm, kernel=3, sweep=1))
             assert np.array_equal(h3[0], half[0]) and np.array_equal(h3[1], half[1]), "fp16 kernel 3 differs"
             del W16d, n16, h3
             torch.cuda.empty_cache()
@@ -225,7 +233,8 @@ def test_config4_sample_over_both_batches():
 def test_config5_first_middle_and_last_batches():
     # topic workload, 27 batches of 1,000,000 documents (the last 900,000):
     # batches 0, 13 and 26, clustered, automatic launch (kernel 3 with
-    # 64-document super-tiles); batch 26 also runs kernel 1 for identical bits
+    # 64-document super-tiles, rotated sweep); batch 26 also runs kernel 1
+    # and kernel 3's ascending sweep for identical bits
     P = _Pass(5)
     bad = []
     for b in (0, 13, 26):
@@ -234,8 +243,9 @@ def test_config5_first_middle_and_last_batches():
         bmu, dist = P.search(ip, ix, perm)
         if b == 26:
             b1, d1 = P.search(ip, ix, perm, kernel=1)
-            assert torch.equal(b1, bmu) and torch.equal(d1, dist), "kernel 1 differs from kernel 3"
-            del b1, d1
+            b3, d3 = P.search(ip, ix, perm, sweep=1)
+            assert torch.equal(b1, b3) and torch.equal(d1, d3), "kernel 1 differs from kernel 3"
+            del b1, d1, b3, d3
         bmu, dist = _host(bmu, dist)
         _distance_property(P.W, P.norms64, indptr, indices, bmu.astype(np.int64), dist.astype(np.float64))
         docs = _sample(len(indptr) - 1, (SAMPLE + 2) // 3, seed=500 + b)

@@ -131,11 +131,21 @@ def test_f16_equals_fp32_search_of_the_widened_codebook():
     indptr, indices = documents(2, 0, n_docs=3000)
     rng = np.random.default_rng(4)
     perm = rng.permutation(3000)
-    ref = _run(W16, indptr, indices, top2=True, dtype=np.float32, ldw=som.som_codebook_ldw(4100))
+    # ascending sweeps: every fp16 kernel and knob gives the fp32 search's bits
+    ref = _run(W16, indptr, indices, top2=True, dtype=np.float32, ldw=som.som_codebook_ldw(4100), sweep=1)
     for knobs in KNOBS16:
         for p in (None, perm):
-            out = _run(W16, indptr, indices, top2=True, perm=p, ldw=som.som_codebook_ldw(4100), **knobs)
+            out = _run(W16, indptr, indices, top2=True, perm=p, ldw=som.som_codebook_ldw(4100),
+                       **{**knobs, "sweep": 1})
             for a, b in zip(out, ref):
+                assert np.array_equal(a, b), knobs
+    # kernel 3's rotated sweep takes the same order for both storage types
+    for knobs in (dict(kernel=3), dict(kernel=3, tile_docs=128)):
+        for p in (None, perm):
+            r32 = _run(W16, indptr, indices, top2=True, perm=p, dtype=np.float32, ldw=som.som_codebook_ldw(4100),
+                       **knobs)
+            r16 = _run(W16, indptr, indices, top2=True, perm=p, ldw=som.som_codebook_ldw(4100), **knobs)
+            for a, b in zip(r16, r32):
                 assert np.array_equal(a, b), knobs
 
 
@@ -185,8 +195,10 @@ def test_f16_planned_search_shares_the_fp32_plan():
     n16 = som.som_codebook_norms(W16d, N=2048)
     assert torch.equal(n32, n16)
     ref = None
-    for knobs in (dict(), dict(kernel=3), dict(kernel=3, tile_docs=128)):
-        # kernel 3: the same super-tile plan for both storage types
+    for knobs in (dict(), dict(kernel=3), dict(kernel=3, tile_docs=128), dict(sweep=1),
+                  dict(kernel=3, tile_docs=128, sweep=1)):
+        # kernel 3: the same super-tile plan for both storage types (and with
+        # the ascending sweep the same bits for every super-tile size)
         plan = som.som_plan(ip, ix, 20000, **knobs)
         a = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W32d, n32, ip, plan, N=2048)]
         b = [t.cpu().numpy() for t in som.som_bmu_search_top2_planned(W16d, n16, ip, plan, N=2048)]
@@ -194,6 +206,7 @@ def test_f16_planned_search_shares_the_fp32_plan():
         for x, y in zip(a, b):
             assert np.array_equal(x, y), knobs
         assert np.array_equal(c[0], a[0]) and np.array_equal(c[1], a[1]), knobs
-        ref = a if ref is None else ref
-        for x, y in zip(a, ref):
-            assert np.array_equal(x, y), knobs
+        if knobs.get("sweep") == 1:
+            ref = a if ref is None else ref
+            for x, y in zip(a, ref):
+                assert np.array_equal(x, y), knobs

@@ -145,7 +145,8 @@ def test_dyadic_codebook_bit_exact_with_ties(N):
                   dict(kernel=2), dict(kernel=2, group_tiles=4, slice_neurons=64),
                   dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256),
                   dict(kernel=3, mask_mode=2), dict(kernel=3, tile_docs=256, mask_mode=2),
-                  dict(kernel=3, schedule=2), dict(kernel=3, tile_docs=128, mask_mode=1, schedule=2)):
+                  dict(kernel=3, schedule=2), dict(kernel=3, tile_docs=128, mask_mode=1, schedule=2),
+                  dict(kernel=3, sweep=1), dict(kernel=3, tile_docs=128, sweep=2)):
         bmu, dist, _ = _search(W, indptr, indices, **knobs)
         assert bmu.tolist() == [e[2][0] for e in exact]
         assert [Fraction(float(x)) for x in dist] == [Fraction(e[1], 16) for e in exact]
@@ -257,7 +258,8 @@ def test_config1_every_document():
     W = codebook(1)
     indptr, indices = documents(1, 0)
     for knobs in (dict(kernel=1, tile_docs=1), dict(kernel=1, tile_docs=8), dict(kernel=2),
-                  dict(kernel=2, group_tiles=4, slice_neurons=64), dict(kernel=3), dict(kernel=3, tile_docs=256)):
+                  dict(kernel=2, group_tiles=4, slice_neurons=64), dict(kernel=3), dict(kernel=3, tile_docs=256),
+                  dict(kernel=3, sweep=1)):
         bmu, dist, _ = _search(W, indptr, indices, **knobs)
         W64 = W.astype(np.float64)
         _check_docs(W64, oracle.codebook_norms(W64), indptr, indices, bmu, dist, range(len(indptr) - 1))
@@ -268,17 +270,30 @@ def test_config2_first_batch():
     W = codebook(2)
     indptr, indices = documents(2, 0)                   # 65,536 documents
     B = len(indptr) - 1
-    bmu, dist, _ = _search(W, indptr, indices, ldw=som.som_codebook_ldw(W.shape[1]))
-    # the benchmark's launch configuration for this map (kernel 3, 64-document
-    # super-tiles, clustered): bit-identical on the whole batch
+    ldw = som.som_codebook_ldw(W.shape[1])
+    # the benchmark's launch for this map: automatic (kernel 3, 64-document
+    # super-tiles, rotated sweep) on the clustered order
     perm = oracle.cluster_order(indptr, indices, W.shape[0])
-    b3, d3, _ = _search(W, indptr, indices, ldw=som.som_codebook_ldw(W.shape[1]), perm=perm, kernel=3)
-    assert np.array_equal(b3, bmu) and np.array_equal(d3, dist)
+    bmu, dist, _ = _search(W, indptr, indices, ldw=ldw, perm=perm)
+    # ascending sweeps: kernel 3 on the clustered order and kernel 1 on the
+    # input order give the same bits on the whole batch
+    b1, d1, _ = _search(W, indptr, indices, ldw=ldw, kernel=1)
+    b3, d3, _ = _search(W, indptr, indices, ldw=ldw, perm=perm, kernel=3, sweep=1)
+    assert np.array_equal(b3, b1) and np.array_equal(d3, d1)
+    # the rotated sweep sums in another order: some distances differ in
+    # rounding (so the rotation is in effect), all by a few ulp at most
+    assert not np.array_equal(dist, d1)
+    assert np.all(np.abs(dist.astype(np.float64) - d1) <= 1e-6 * np.abs(d1.astype(np.float64)))
     W64 = W.astype(np.float64)
     norms64 = oracle.codebook_norms(W64)
     rng = np.random.default_rng(0)
     sample = np.unique(np.concatenate([[0, B - 1], rng.choice(B, 1500, replace=False)]))
     _check_docs(W64, norms64, indptr, indices, bmu, dist, sample)
+    # where the two sweeps pick different neurons, both must be in the oracle's near-tie band
+    flips = np.nonzero(b1 != bmu)[0]
+    assert len(flips) <= 20, len(flips)
+    _check_docs(W64, norms64, indptr, indices, bmu, dist, flips)
+    _check_docs(W64, norms64, indptr, indices, b1, d1, flips)
     # every document: the reported distance is the distance of the reported neuron
     nnz = np.diff(indptr)
     g = np.repeat(bmu, nnz)
@@ -288,8 +303,9 @@ def test_config2_first_batch():
 
 
 def test_results_identical_across_tile_chunk_and_order():
-    """Each document's dot product is summed in ascending feature order
-    whatever the tiling, so the outputs are bit-identical."""
+    """With the ascending sweep each document's dot product is summed in
+    ascending feature order whatever the tiling, so the outputs are
+    bit-identical."""
     from synth import codebook, documents
     W = codebook(2, N=4100, F=20000)
     indptr, indices = documents(2, 0, n_docs=3000)
@@ -300,14 +316,15 @@ def test_results_identical_across_tile_chunk_and_order():
     for T in TILES:
         for K, G, mode in ((0, 0, 0), (4, 1, 1), (8 if T < 32 else 4, 8, 2), (4, 2, 2)):
             variants.append(dict(kernel=1, tile_docs=T, lane_neurons=K, group_tiles=G, mask_mode=mode))
-    variants += [dict(kernel=3, tile_docs=D, mask_mode=m) for D in SUPER for m in (1, 2)]
+    variants += [dict(kernel=3, tile_docs=D, mask_mode=m, sweep=1) for D in SUPER for m in (1, 2)]
     # schedule chunks of the neuron axis (17 slices of 256 neurons here: full
     # and partial last chunks, and one chunk wider than the map)
     variants += [dict(kernel=1, neuron_chunk=nc) for nc in (512, 768, 4096, 1 << 20)]
     variants += [dict(kernel=1, tile_docs=16, group_tiles=4, neuron_chunk=768),
                  dict(kernel=1, lane_neurons=8, neuron_chunk=1024)]
     variants += [dict(kernel=3, neuron_chunk=nc) for nc in (512, 768, 4096)]
-    variants += [dict(kernel=3, tile_docs=128, neuron_chunk=512), dict(kernel=3, mask_mode=1, neuron_chunk=1024)]
+    variants += [dict(kernel=3, tile_docs=128, neuron_chunk=512), dict(kernel=3, mask_mode=1, neuron_chunk=1024),
+                 dict(kernel=3, neuron_chunk=256, sweep=1), dict(kernel=3, schedule=2)]
     for i, v in enumerate(variants):
         for perm in perms if (i % 5 == 0 or v["kernel"] == 3) else perms[:2]:
             out = _search(W, indptr, indices, perm=perm, **v)
@@ -316,7 +333,7 @@ def test_results_identical_across_tile_chunk_and_order():
             assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), v
     # the row stride is a layout choice only
     for ldw in (som.som_codebook_ldw(4100), 4104, 4100 + 1024):
-        for v in (dict(), dict(kernel=1, lane_neurons=8), dict(kernel=2), dict(kernel=3)):
+        for v in (dict(sweep=1), dict(kernel=1, lane_neurons=8), dict(kernel=2), dict(kernel=3, sweep=1)):
             out = _search(W, indptr, indices, ldw=ldw, **v)
             assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (ldw, v)
 
@@ -329,6 +346,44 @@ def test_repeated_runs_are_bit_identical():
     for _ in range(3):
         b = _search(W, indptr, indices)
         assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_rotated_sweep_order_is_fixed_and_within_tolerance():
+    """Kernel 3's rotated sweep (its automatic order): the order depends on the
+    plan and the launch's tile grid only, so the results are the same across
+    repeated calls, row strides, planned and unplanned searches, top-2 and
+    one-slice schedule chunks; they differ from the ascending sweep's only in
+    rounding (some distances do differ: the rotation is in effect), and both
+    are accepted by the oracle on every document."""
+    from synth import codebook, documents
+    W = codebook(2, N=4100, F=20000)
+    indptr, indices = documents(2, 0, n_docs=3000)
+    perm = oracle.cluster_order(indptr, indices, 20000)
+    W64 = W.astype(np.float64)
+    norms64 = oracle.codebook_norms(W64)
+    for D in SUPER:
+        ref = _search(W, indptr, indices, perm=perm, kernel=3, tile_docs=D)
+        for v in (dict(sweep=2), dict(neuron_chunk=256), dict(sweep=2, neuron_chunk=256)):
+            out = _search(W, indptr, indices, perm=perm, kernel=3, tile_docs=D, **v)
+            assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (D, v)
+        for ldw in (4104, 4100 + 1024):
+            out = _search(W, indptr, indices, perm=perm, ldw=ldw, kernel=3, tile_docs=D)
+            assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (D, ldw)
+        Wd, _ = _dev_W(W)
+        norms = som.som_codebook_norms(Wd, N=4100)
+        ip, ix, pd = _dev_i32(indptr), _dev_i32(indices), _dev_i32(perm)
+        plan = som.som_plan(ip, ix, 20000, perm=pd, kernel=3, tile_docs=D)
+        pl = som.som_bmu_search_planned(Wd, norms, ip, plan, N=4100)
+        t2 = som.som_bmu_search_top2(Wd, norms, ip, ix, N=4100, perm=pd, kernel=3, tile_docs=D)
+        torch.cuda.synchronize()
+        for b, d in (pl, t2[:2]):
+            assert np.array_equal(b.cpu().numpy(), ref[0]) and np.array_equal(d.cpu().numpy(), ref[1]), D
+        asc = _search(W, indptr, indices, perm=perm, kernel=3, tile_docs=D, sweep=1)
+        assert not np.array_equal(asc[1], ref[1]), D
+        rel = np.abs(asc[1].astype(np.float64) - ref[1]) / np.abs(asc[1].astype(np.float64))
+        assert rel.max() <= 1e-6, (D, rel.max())
+        _check_docs(W64, norms64, indptr, indices, ref[0], ref[1], range(3000))
+        del Wd, norms, plan
 
 
 # ----------------------------------------------------------------------------
@@ -558,8 +613,9 @@ def test_planned_search_reuses_a_plan_across_codebooks():
     indptr, indices = documents(1, 0, n_docs=2500)
     ip, ix = _dev_i32(indptr), _dev_i32(indices)
     perm = _dev_i32(oracle.cluster_order(indptr, indices, 2048))
-    plan = som.som_plan(ip, ix, 2048, perm=perm)
+    plan = som.som_plan(ip, ix, 2048, perm=perm, sweep=1)       # kernel 3, ascending sweep
     plan1 = som.som_plan(ip, ix, 2048, perm=perm, kernel=1, tile_docs=4)
+    planr = som.som_plan(ip, ix, 2048, perm=perm)                # kernel 3, rotated sweep
     for seed in (0, 1):
         W = codebook(1, seed=seed)
         Wd, _ = _dev_W(W)
@@ -567,7 +623,10 @@ def test_planned_search_reuses_a_plan_across_codebooks():
         a = som.som_bmu_search_planned(Wd, norms, ip, plan)
         b = som.som_bmu_search(Wd, norms, ip, ix, perm=perm, kernel=1, tile_docs=4)
         c = som.som_bmu_search_planned(Wd, norms, ip, plan1)
+        r = som.som_bmu_search_planned(Wd, norms, ip, planr)
+        r0 = som.som_bmu_search(Wd, norms, ip, ix, perm=perm)
         torch.cuda.synchronize()
+        assert torch.equal(r[0], r0[0]) and torch.equal(r[1], r0[1])
         assert torch.equal(a[0], c[0]) and torch.equal(a[1], c[1])
         torch.cuda.synchronize()
         assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])

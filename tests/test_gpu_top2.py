@@ -138,26 +138,39 @@ def test_top2_agrees_with_plain_search_and_across_knobs():
     Wd = _dev_W(W, som.som_codebook_ldw(4100))
     norms = som.som_codebook_norms(Wd, N=4100)
     ip, ix = _i32(indptr), _i32(indices)
-    b0, d0 = [t.cpu().numpy() for t in som.som_bmu_search(Wd, norms, ip, ix, N=4100)]
+    # ascending sweeps: every kernel, knob and tile order gives the same bits
+    b0, d0 = [t.cpu().numpy() for t in som.som_bmu_search(Wd, norms, ip, ix, N=4100, sweep=1)]
     ref = None
     for i, knobs in enumerate(KNOBS):
         for p in perms if i % 3 == 0 else perms[:2]:
             pd = None if p is None else _i32(p)
-            out = [t.cpu().numpy() for t in som.som_bmu_search_top2(Wd, norms, ip, ix, N=4100, perm=pd, **knobs)]
+            out = [t.cpu().numpy() for t in som.som_bmu_search_top2(Wd, norms, ip, ix, N=4100, perm=pd,
+                                                                    **{**knobs, "sweep": 1})]
             assert np.array_equal(out[0], b0) and np.array_equal(out[1], d0), knobs
             if ref is None:
                 ref = out
             assert np.array_equal(out[2], ref[2]) and np.array_equal(out[3], ref[3]), knobs
+    # the rotated sweep (kernel 3's automatic order): the first place equals
+    # the plain search's with the same plan, the pair is accepted by the oracle
+    rot = {}
+    for knobs in (dict(), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256)):
+        for p in perms:
+            pd = None if p is None else _i32(p)
+            out = [t.cpu().numpy() for t in som.som_bmu_search_top2(Wd, norms, ip, ix, N=4100, perm=pd, **knobs)]
+            pb, pdist = [t.cpu().numpy() for t in som.som_bmu_search(Wd, norms, ip, ix, N=4100, perm=pd, **knobs)]
+            assert np.array_equal(out[0], pb) and np.array_equal(out[1], pdist), knobs
+            rot[len(rot)] = out
     # against the oracle's second place, on a sample
     W64 = W.astype(np.float64)
     norms64 = oracle.codebook_norms(W64)
     bad = []
     for d in np.unique(np.concatenate([[0, 2999], rng.choice(3000, 400, replace=False)])):
         feats = indices[indptr[d]:indptr[d + 1]].astype(np.int64)
-        ok, why = oracle.accept_top2(W64, norms64, feats, int(ref[0][d]), float(ref[1][d]), int(ref[2][d]),
-                                     float(ref[3][d]), REL)
-        if not ok:
-            bad.append((int(d), why))
+        for o in [ref] + list(rot.values()):
+            ok, why = oracle.accept_top2(W64, norms64, feats, int(o[0][d]), float(o[1][d]), int(o[2][d]),
+                                         float(o[3][d]), REL)
+            if not ok:
+                bad.append((int(d), why))
     assert not bad, bad[:5]
 
 

@@ -43,7 +43,7 @@ def _both(W, indptr, indices, block_docs, perm=None, ldw=None, **knobs):
     norms = som.som_codebook_norms(Wd, N=N)
     ip, ix = _i32(indptr), _i32(indices)
     p = None if perm is None else _i32(perm)
-    fused = som.som_bmu_search(Wd, norms, ip, ix, N=N, perm=p, **knobs)
+    fused = som.som_bmu_search(Wd, norms, ip, ix, N=N, perm=p, **{"sweep": 1, **knobs})   # ascending, as kernel 1
     unf = som.som_bmu_search_unfused(Wd, norms, ip, ix, N=N, perm=p, block_docs=block_docs, **knobs)
     torch.cuda.synchronize()
     return [t.cpu().numpy() for t in fused], [t.cpu().numpy() for t in unf]
