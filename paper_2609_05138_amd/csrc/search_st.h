@@ -89,6 +89,48 @@ __device__ __forceinline__ void wait_stages(int n) {
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
+// The adds of a stage for a wave's eight documents, fp32 rows,
+// document-major dispatch: w[j] holds the stage words of documents 2j (low
+// half) and 2j + 1 (high half); for each set bit r of a document's word, in
+// ascending order, the lane's 16 bytes of row r of the stage's LDS slot (at
+// byte vbase + 1024 r) are added to that document's four accumulators.  One
+// inline-assembly statement keeps the loop at three scalar instructions per
+// row and each document's test at one: the compiler's form compares each
+// cleared word with zero again after the s_and that has already set SCC,
+// tests a half-word in two instructions, and pads every statement boundary
+// with a wait state.  The row lands in v60-v63, which the statement clobbers.
+#define SOM_DOC_ROWS(FIRST, D)                         \
+  FIRST "\n\t"                                         \
+  "s_cbranch_scc0 7f\n"                                 \
+  "9:\n\t"                                             \
+  "s_ff1_i32_b32 %[r], %[dm]\n\t"                      \
+  "v_lshl_add_u32 %[va], %[r], 10, %[vb]\n\t"          \
+  "ds_read_b128 v[60:63], %[va]\n\t"                   \
+  "s_add_i32 %[r], %[dm], -1\n\t"                      \
+  "s_and_b32 %[dm], %[dm], %[r]\n\t"                   \
+  "s_waitcnt lgkmcnt(0)\n\t"                           \
+  "v_add_f32_e32 %[" #D "0], v60, %[" #D "0]\n\t"      \
+  "v_add_f32_e32 %[" #D "1], v61, %[" #D "1]\n\t"      \
+  "v_add_f32_e32 %[" #D "2], v62, %[" #D "2]\n\t"      \
+  "v_add_f32_e32 %[" #D "3], v63, %[" #D "3]\n\t"      \
+  "s_cbranch_scc1 9b\n"                                \
+  "7:\n\t"
+#define SOM_DOC_ACC(D, A) [D##0] "+v"(A[0]), [D##1] "+v"(A[1]), [D##2] "+v"(A[2]), [D##3] "+v"(A[3])
+__device__ __forceinline__ void add_stage_8docs_f32(float (&acc)[8][4], const uint32_t (&w)[4], uint32_t vbase) {
+  uint32_t dm, r, va;
+  asm volatile(SOM_DOC_ROWS("s_and_b32 %[dm], %[w0], 0xffff", a) SOM_DOC_ROWS("s_lshr_b32 %[dm], %[w0], 16", b)
+               SOM_DOC_ROWS("s_and_b32 %[dm], %[w1], 0xffff", c) SOM_DOC_ROWS("s_lshr_b32 %[dm], %[w1], 16", d)
+               SOM_DOC_ROWS("s_and_b32 %[dm], %[w2], 0xffff", e) SOM_DOC_ROWS("s_lshr_b32 %[dm], %[w2], 16", f)
+               SOM_DOC_ROWS("s_and_b32 %[dm], %[w3], 0xffff", g) SOM_DOC_ROWS("s_lshr_b32 %[dm], %[w3], 16", h)
+               : SOM_DOC_ACC(a, acc[0]), SOM_DOC_ACC(b, acc[1]), SOM_DOC_ACC(c, acc[2]),
+                 SOM_DOC_ACC(d, acc[3]), SOM_DOC_ACC(e, acc[4]), SOM_DOC_ACC(f, acc[5]),
+                 SOM_DOC_ACC(g, acc[6]), SOM_DOC_ACC(h, acc[7]), [dm] "=&s"(dm), [r] "=&s"(r), [va] "=&v"(va)
+               : [w0] "s"(w[0]), [w1] "s"(w[1]), [w2] "s"(w[2]), [w3] "s"(w[3]), [vb] "v"(vbase)
+               : "v60", "v61", "v62", "v63", "scc", "memory");
+}
+#undef SOM_DOC_ACC
+#undef SOM_DOC_ROWS
+
 // Dispatch of a stage's rows to a wave's documents (both add every row in
 // ascending feature order, so their results are bit-identical):
 //   kStRowMajor: visit each entry some document of the wave holds (one
@@ -256,6 +298,84 @@ k_search_st(SearchArgs a) {
         SOM_ST_ISSUE(q, fid)
       }
     }
+    if constexpr (DOC) {
+      static_assert(NSLOT == 2, "document-major: a two-slot ring");
+      // LDS byte offsets of the slot being added (the other slot receives the
+      // next stage): 0 or one slot, swapped after every stage
+      constexpr uint32_t kRingSlot = P * 1024, kMaskSlot = S * 256;
+      uint32_t rcur = 0, mcur = 0;
+      const uint32_t ring_lane = lds_offset(&ring[0][0][lane]);
+      const uint32_t mring_lane = lds_offset(&mring[0][wave][lane]);
+      // this wave's adds of the stage in the slot at ring offset rb
+      auto add_stage = [&](uint32_t rb) {
+        uint32_t cur[SW];
+#pragma unroll
+        for (int k = 0; k < SW; ++k) cur[k] = dmw[k];
+        if constexpr (sizeof(WT) == 4 && K == 4 && T == 8) {
+          const uint32_t vbase = ring_lane + rb;
+          add_stage_8docs_f32(acc, cur, vbase);
+        } else {
+          const int slot = rb ? 1 : 0;
+#pragma unroll
+          for (int sd = 0; sd < T; ++sd) {
+            // the entries of the stage that document sd of this wave holds
+            uint32_t dm = (cur[sd >> 1] >> ((sd & 1) * 16)) & 0xffffu;
+            while (dm) {
+              const int r = __builtin_ctz(dm);
+              dm &= dm - 1;
+              float4 wf[K / 4];
+              widen_v<WT>(ring[slot][r][lane], wf);
+#pragma unroll
+              for (int qq = 0; qq < K / 4; ++qq) {
+                acc[sd][4 * qq + 0] += wf[qq].x;
+                acc[sd][4 * qq + 1] += wf[qq].y;
+                acc[sd][4 * qq + 2] += wf[qq].z;
+                acc[sd][4 * qq + 3] += wf[qq].w;
+              }
+            }
+          }
+        }
+      };
+      // every stage but the last issues the next one; the last is peeled off
+      for (int32_t s = 0; s + 1 < nstages; ++s) {
+        vm_wait<0>();   // this wave's loads of stage s have landed
+        lds_barrier();  // stage s visible to all waves; every wave is done with stage s-1
+        const uint32_t w = *reinterpret_cast<const __attribute__((address_space(3))) uint32_t*>(
+            static_cast<uintptr_t>(mring_lane + mcur));
+        // the next stage: its rows' byte offsets computed once on the id
+        // lanes (lane P + r holds entry r's feature id; past the union: row
+        // 0), then moved to scalar registers one row at a time
+        const int32_t qa = ROT ? a1 : s + 1;
+        const bool live = id_lane && qa * P + (lane - P) < cnt;
+        const uint64_t off = static_cast<uint64_t>(w & (live ? ~0u : 0u)) * static_cast<uint64_t>(ldw_b);
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+          const int src = P + wave * RPW + i;
+          const uint64_t o = (static_cast<uint64_t>(static_cast<uint32_t>(
+                                 __builtin_amdgcn_readlane(static_cast<int>(off >> 32), src))) << 32) |
+                             static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), src));
+          dma_b128(Wn + o, ring0 + (kRingSlot - rcur) + static_cast<uint32_t>(i * 1024));
+        }
+        if (id_mine) dma_b32(ROT ? idl + a2 * P : dsrc + (s + 1) * dstride, mring0 + (kMaskSlot - mcur));
+        add_stage(rcur);
+        // the next stage's words, loaded now (their wait falls on the next
+        // stage's first LDS read, after its barrier)
+#pragma unroll
+        for (int k = 0; k < SW; ++k)
+          dmw[k] = reinterpret_cast<const_u32>(reinterpret_cast<const __attribute__((address_space(4))) char*>(smask) +
+                                              static_cast<uint32_t>(qa) * (P * MW * 4))[k];
+        if (ROT) {
+          const int32_t n2 = a2 + 1;
+          a1 = a2;
+          a2 = n2 == nstages ? 0 : n2;
+        }
+        rcur = kRingSlot - rcur;
+        mcur = kMaskSlot - mcur;
+      }
+      vm_wait<0>();
+      lds_barrier();
+      add_stage(rcur);
+    } else {
     for (int32_t s = 0; s < nstages; ++s) {
       // this wave's stages issued after s: min(nstages - 1, s + NSLOT - 2) - s
       const int32_t later = (nstages - 1 < s + NSLOT - 2 ? nstages - 1 : s + NSLOT - 2) - s;
@@ -265,62 +385,10 @@ k_search_st(SearchArgs a) {
       const uint32_t w = mring[slot][wave][lane];
       if (s + NSLOT - 1 < nstages) {
         const int32_t q = s + NSLOT - 1;
-        if (DOC) {
-          // byte offsets of stage q's rows, computed once on the id lanes
-          // (lane P + r holds entry r's feature id; past the union: row 0),
-          // then moved to scalar registers one row at a time
-          const bool live = id_lane && (ROT ? a1 : q) * P + (lane - P) < cnt;
-          const uint64_t off = static_cast<uint64_t>(live ? w : 0u) * static_cast<uint64_t>(ldw_b);
-          const uint32_t slot_ = static_cast<uint32_t>(q % NSLOT);
+        int32_t fid[RPW];
 #pragma unroll
-          for (int i = 0; i < RPW; ++i) {
-            const int src = P + wave * RPW + i;
-            const uint64_t o = (static_cast<uint64_t>(static_cast<uint32_t>(
-                                   __builtin_amdgcn_readlane(static_cast<int>(off >> 32), src))) << 32) |
-                               static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), src));
-            dma_b128(Wn + o, ring0 + slot_ * (P * 1024) + static_cast<uint32_t>(i * 1024));
-          }
-          if (id_mine) dma_b32(ROT ? idl + a2 * P : dsrc + q * dstride, mring0 + slot_ * (S * 256));
-        } else {
-          int32_t fid[RPW];
-#pragma unroll
-          for (int i = 0; i < RPW; ++i) fid[i] = __builtin_amdgcn_readlane(static_cast<int>(w), P + wave * RPW + i);
-          SOM_ST_ISSUE(q, fid)
-        }
-      }
-      if (DOC) {
-        uint32_t cur[SW];
-#pragma unroll
-        for (int k = 0; k < SW; ++k) cur[k] = dmw[k];
-#pragma unroll
-        for (int sd = 0; sd < T; ++sd) {
-          // the entries of stage s that document sd of this wave holds
-          uint32_t dm = (cur[sd >> 1] >> ((sd & 1) * 16)) & 0xffffu;
-          while (dm) {
-            const int r = __builtin_ctz(dm);
-            dm &= dm - 1;
-            float4 wf[K / 4];
-            widen_v<WT>(ring[slot][r][lane], wf);
-#pragma unroll
-            for (int qq = 0; qq < K / 4; ++qq) {
-              acc[sd][4 * qq + 0] += wf[qq].x;
-              acc[sd][4 * qq + 1] += wf[qq].y;
-              acc[sd][4 * qq + 2] += wf[qq].z;
-              acc[sd][4 * qq + 3] += wf[qq].w;
-            }
-          }
-        }
-        // the next stage's words, loaded now (their wait falls on the next
-        // stage's first LDS read, after its barrier)
-        if (s + 1 < nstages) {
-#pragma unroll
-          for (int k = 0; k < SW; ++k) dmw[k] = smask[(ROT ? a1 : s + 1) * P * MW + k];
-        }
-        if (ROT) {
-          a1 = a2;
-          a2 = a2 + 1 >= nstages ? a2 + 1 - nstages : a2 + 1;
-        }
-        continue;
+        for (int i = 0; i < RPW; ++i) fid[i] = __builtin_amdgcn_readlane(static_cast<int>(w), P + wave * RPW + i);
+        SOM_ST_ISSUE(q, fid)
       }
       const uint32_t m_cur = (lane < P && s * P + lane < cnt) ? (w >> mshift) & kWaveBits : 0u;
       // this wave's needed entries of stage s, visited in ascending order
@@ -345,6 +413,7 @@ k_search_st(SearchArgs a) {
         widen_v<WT>(cur, wf);
         add_row<T, K, kMaskBranch>(acc, wf, mc);
       }
+    }
     }
 #undef SOM_ST_ISSUE
   }
