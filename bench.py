@@ -44,6 +44,7 @@ if ROOT not in sys.path:
 L2_PEAK_BPS = 8 * 16 * 128 * 2.4e9
 HBM_PEAK_BPS = 8.0e12
 VALU_PEAK_ADDS = 256 * 128 * 2.4e9       # 256 CUs x 128 fp32 lanes/clk x 2.4 GHz
+LDS_PEAK_BPS = 256 * 128 * 2.4e9         # 256 CUs x 128 B/clk x 2.4 GHz (derived)
 REL = 1e-5
 
 # Fabric (memory-side cache + HBM) bytes read and written per search launch,
@@ -650,6 +651,11 @@ def main():
               "compulsory_hbm_vs_hbm_peak": comp_rate / HBM_PEAK_BPS}
     if probes:
         levels["l2_algorithmic_vs_measured_l2"] = l2_rate / (probes["l2_GBps"] * 1e9)
+    if kernel == 3 and not args.unfused:
+        # kernel 3 writes every union row slice into LDS once per super-tile
+        # (direct-to-LDS loads) and reads it from LDS once per membership
+        lds_bytes = (float(sum(nnzs)) + float(union_total)) * N * wbytes
+        levels["lds_algorithmic_vs_derived_lds_peak"] = lds_bytes / float(np.sum(search_s)) / LDS_PEAK_BPS
     if traffic is not None:
         fab = traffic * len(batches) / float(np.sum(search_s))
         levels["fabric_measured_vs_hbm_peak"] = fab / HBM_PEAK_BPS
