@@ -386,6 +386,33 @@ def test_rotated_sweep_order_is_fixed_and_within_tolerance():
         del Wd, norms, plan
 
 
+def test_rotated_sweep_exact_on_a_dyadic_codebook():
+    """Rotated sweeps with long unions and many super-tiles per XCD (so the
+    super-tiles start at nonzero stages and wrap round, ragged last stages
+    included): on a dyadic codebook every fp32 sum is exact, so whatever the
+    order each index (lowest on ties) and distance must equal the exact
+    integer evaluation; a skipped or repeated row would not."""
+    rng = np.random.default_rng(31)
+    F, N, B = 2000, 61, 10240
+    K = rng.integers(0, 4, (F, N))
+    K[:, 60] = K[:, 7]                                  # exact duplicate neurons -> ties
+    W = K.astype(np.float32) / 4
+    nnz = rng.poisson(40, B).clip(1, 200)
+    nnz[::97] = 0                                       # some empty documents
+    indptr = np.concatenate([[0], np.cumsum(nnz)])
+    indices = np.concatenate([np.sort(rng.choice(F, k, replace=False)) for k in nnz])
+    exact = oracle.bmu_search_exact(K, 2, indptr, indices)
+    want_b = [e[0] for e in exact]
+    want_d = [Fraction(e[1], 16) for e in exact]
+    perm = oracle.cluster_order(indptr, indices, F)
+    for knobs in (dict(), dict(sweep=2), dict(tile_docs=128), dict(sweep=2, neuron_chunk=256),
+                  dict(sweep=1), dict(kernel=1)):
+        for p in (None, perm):
+            bmu, dist, _ = _search(W, indptr, indices, perm=p, **knobs)
+            assert bmu.tolist() == want_b, knobs
+            assert [Fraction(float(x)) for x in dist] == want_d, knobs
+
+
 # ----------------------------------------------------------------------------
 # edge cases
 # ----------------------------------------------------------------------------
