@@ -23,16 +23,18 @@
 // vector-memory count: the loads of the later stages may stay in flight),
 // then one barrier makes every wave's part visible and closes stage s-1,
 // whose slot the loads of stage s+NSLOT-1 then reuse.  The feature ids of
-// those loads arrive with stage s itself (spare lanes of its mask load).  Entries past the
-// union's end load row 0 and get empty masks.  A wave adds only the entries
-// of a stage its documents hold, in one of two dispatch forms (StDispatch
-// below): row-major (a ballot over the stage's entry masks gives the needed
-// rows, visited in ascending order with the next row's LDS read issued
-// before the current row's adds) or document-major (the default: per
-// document, the stage entries it holds, from 16-bit document words that the
-// plan stores per stage and the wave reads with scalar loads a stage ahead).
+// those loads arrive with stage s itself (spare lanes of its mask load).
+// Entries past the union's end load row 0 and get empty masks.  A wave adds
+// only the entries of a stage its documents hold, in one of the dispatch
+// forms of StDispatch below: row-major (a ballot over the stage's entry
+// masks gives the needed rows, visited in ascending order with the next
+// row's LDS read issued before the current row's adds) or document-major
+// (per document, the stage entries it holds, from 16-bit document words that
+// the plan stores per stage and the wave reads with scalar loads a stage
+// ahead; for fp32 rows the whole stage's adds are one inline-assembly
+// statement, and the last stage is peeled off the loop).
 //
-// Rotated sweep (the third dispatch form): each super-tile starts its union
+// Rotated sweep (the default document-major form): each super-tile starts its union
 // at a stage chosen from its place in its XCD's work and wraps round, so that
 // the super-tiles an XCD runs at once sweep the same part of the feature
 // range at the same time and share their rows in that XCD's L2 (in ascending
