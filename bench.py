@@ -58,8 +58,8 @@ MEASURED_TRAFFIC = {
     json.dumps(["map512x512-F20000-2M", [0, 1], 0, 262208, "f32", False, False, False, False,
                 {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
                  "schedule": 0, "slice_neurons": 0, "storage": 0, "sweep": 0, "tile_docs": 0}]): {
-        "csrc": "681686af88e43215",
-        "fetch_kib": [5.3777e9, 4.8299e9],       # per search launch (batch 0, batch 1)
+        "csrc": "6892385d1fb5cec3",
+        "fetch_kib": [5.3862e9, 4.8464e9],       # per search launch (batch 0, batch 1)
         "write_kib": [3.3554e7, 3.0446e7],
         "fetch_scale": 2.0, "write_scale": 1.0,   # plain 4 GiB device copy: FETCH_SIZE reads half, WRITE_SIZE exact
         "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,2>, "
@@ -69,8 +69,8 @@ MEASURED_TRAFFIC = {
     json.dumps(["map512x512-F20000-26.9M-topics", [0], 0, 262208, "f32", False, False, False, False,
                 {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
                  "schedule": 0, "slice_neurons": 0, "storage": 0, "sweep": 0, "tile_docs": 0}]): {
-        "csrc": "681686af88e43215",
-        "fetch_kib": [1.3542e10],
+        "csrc": "6892385d1fb5cec3",
+        "fetch_kib": [1.3539e10],
         "write_kib": [3.2000e7],
         "fetch_scale": 2.0, "write_scale": 1.0,
         "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,2>, "

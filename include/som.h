@@ -56,13 +56,14 @@ typedef enum som_status {
  * the defaults.  Only `sweep` changes a result, and only in rounding: with
  * the ascending sweep every document's dot product is summed in ascending
  * feature order whatever the other knobs, so outputs are bit-identical
- * across all their settings and all kernels; the rotated sweep (kernel 3's
- * default) sums in a rotated order that is fixed for a given batch, perm,
- * opts and device.
+ * across all their settings and all kernels; the rotated sweep (the default
+ * of kernels 1 and 3) sums in a rotated order that is fixed for a given
+ * batch, perm, opts and device.
  *
  * Automatic choices (measured on MI355X at map sizes 32^2 to 512^2, F =
- * 2,048 to 20,000, batches up to 1M documents): for an fp32 codebook kernel
- * 3 with 64-document super-tiles and the document-major dispatch; for fp16,
+ * 2,048 to 20,000, batches up to 1M documents): rotated union sweeps
+ * (`sweep`) wherever available; for an fp32 codebook kernel 3 with
+ * 64-document super-tiles and the document-major dispatch; for fp16,
  * or when a knob only kernel 1 has is set (tile_docs of 32 or less,
  * lane_neurons, group_tiles), kernel 1 with tiles of 16 documents for fp32
  * and 8 for fp16, and four tiles per workgroup for fp32 tiles of 16
@@ -120,19 +121,22 @@ typedef struct som_bmu_opts {
                             tile's slices of the chunk back to back.  Chunks wider than the map
                             cover it whole. */
   int32_t sweep;         /* order of each union sweep: 0 = auto (2 where available, else 1),
-                            1 = ascending feature order, 2 = rotated (kernel 3 with mask_mode 2,
-                            schedule 1 and one-slice chunks only; else SOM_ERR_INVALID_ARG):
-                            each super-tile starts its union at a stage given by its place in
-                            its XCD's share of the launch and wraps round, so that the
-                            super-tiles an XCD runs at once sweep the same feature range
-                            together and share its L2 (measured 19% faster on the topic
-                            workload, neutral on the Zipf maps).  A document's dot product is
-                            then summed in that order, which depends on the plan, the launch's
-                            tile grid and the device's CU count and occupancy, not on the
-                            codebook or the neuron range: results are reproducible on one
-                            device type and column ranges compose exactly, but may differ from
-                            the ascending sweep's in the last bits of dist (and, at exact or
-                            near ties, in bmu). */
+                            1 = ascending feature order, 2 = rotated (kernel 1, or kernel 3 with
+                            mask_mode 2, as one launch of one-slice chunks: schedule 1 and
+                            neuron_chunk 0 or one slice; else SOM_ERR_INVALID_ARG): each tile
+                            (kernel 3: super-tile) starts its union at an entry (a stage) given
+                            by its place in its XCD's share of the launch and wraps round, so
+                            that the tiles an XCD runs at once sweep the same feature range
+                            together and share its L2 (on the topic workload measured 19%
+                            faster with kernel 3 and 17% with fp16 kernel 1; within 1.3% on
+                            the Zipf maps).  A document's dot product is then summed in that
+                            order, which depends on the plan, the launch's tile grid and the
+                            device's CU count, not on the codebook, its storage type or the
+                            neuron range: results are reproducible on one device type, fp16
+                            and fp32 searches of one plan use the same order, and column
+                            ranges compose exactly, but results may differ from the ascending
+                            sweep's in the last bits of dist (and, at exact or near ties, in
+                            bmu). */
 } som_bmu_opts;
 
 /* Version of this ABI (bumped on any incompatible change). */
@@ -332,10 +336,10 @@ som_status som_cluster_order(const int32_t* indptr, const int32_t* indices, int6
  * weights are the fp16 values widened exactly to fp32: norms are the rounded
  * weights' norms (fp64 accumulate, rounded once), and every document's dot
  * product sums the widened weights in the order opts->sweep names, so fp16
- * and fp32 searches of the same (fp16-representable) codebook are
- * bit-identical with the ascending sweep (sweep = 1 for the fp32 search,
- * whose automatic kernel 3 otherwise rotates; the fp16 search's automatic
- * kernel 1 is ascending).  Search knobs: kernels 1 (the automatic one for
+ * and fp32 searches of the same (fp16-representable) codebook with the same
+ * kernel and knobs are bit-identical; across the automatic kernels (3 for
+ * fp32, 1 for fp16, both rotating) they are with the ascending sweep
+ * (sweep = 1).  Search knobs: kernels 1 (the automatic one for
  * fp16) and 3; lane_neurons 0 or 8 (a 512-neuron slice, one 128-bit load of
  * 8 weights per lane per row); tile_docs up to 16 for kernel 1, 64 or 128
  * for kernel 3.  Plans from som_plan are shared with the fp32 search.

@@ -82,9 +82,11 @@ __host__ __device__ inline void chunked_block(uint64_t lin, uint64_t nx, uint64_
   *slice = chunk * q + r % qq;
 }
 
-// Phase period of kernel 3's rotated sweep for super-tiles of S waves of T
-// documents (see search.hip).
+// Phase periods of the rotated sweeps (see search.hip): kernel 3 with
+// super-tiles of S waves of T documents, in workgroups per XCD; kernel 1
+// with T-document tiles, G per workgroup, in tiles per XCD.
 hipError_t st_phase_wgs(int T, int S, int32_t* wgs);
+hipError_t k1_phase_tiles(int T, int G, int mask_mode, int32_t* tiles);
 
 struct SearchArgs {
   const void* W;    // fp32 or fp16 [F][ldw] (see `weights`)
@@ -115,9 +117,9 @@ struct SearchArgs {
   // chunk; the grid's workgroups walk the chunks in turn, and inside a chunk
   // each XCD's tiles with their chunk slices back to back (1 = slice-major)
   int32_t chunk_slices = 1;
-  // kernel 3, document-major, one launch of one-slice chunks: 1 = rotated
-  // sweep; phase_wgs is its phase period in workgroups per XCD (set by the
-  // launch)
+  // kernels 1 and 3 (one launch of one-slice chunks; kernel 3
+  // document-major): 1 = rotated sweep; phase_wgs is its phase period, in
+  // workgroups (kernel 3) or tiles (kernel 1) per XCD, set by the launch
   int32_t rotate = 0;
   int32_t phase_wgs = 0;
   float* score = nullptr;  // unfused comparator: distances of tiled-order documents

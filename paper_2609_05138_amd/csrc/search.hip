@@ -293,6 +293,46 @@ hipError_t st_phase_wgs(int T, int S, int32_t* wgs) {
   return hipSuccess;
 }
 
+// Phase period of kernel 1's rotated sweep, in tiles per XCD: 3/2 of the
+// tiles (one per wave) one XCD holds at once, from the fp32 kernel of the
+// tile shape for both storage types, as for kernel 3.
+template <int T, int G>
+const void* k1_f32_kernel(int mask_mode) {
+  constexpr int U = T >= 16 ? 2 : 8;  // fp32 rows per batch (launch_tkg)
+  return mask_mode == kMaskBranch ? reinterpret_cast<const void*>(k_search<float, T, 4, G, U, kMaskBranch>)
+                                  : reinterpret_cast<const void*>(k_search<float, T, 4, G, U, kMaskFma>);
+}
+template <int T>
+const void* k1_f32_kernel_g(int G, int mask_mode) {
+  switch (G) {
+    case 1: return k1_f32_kernel<T, 1>(mask_mode);
+    case 2: return k1_f32_kernel<T, 2>(mask_mode);
+    case 4: return k1_f32_kernel<T, 4>(mask_mode);
+    case 8: return k1_f32_kernel<T, 8>(mask_mode);
+    default: return nullptr;
+  }
+}
+
+hipError_t k1_phase_tiles(int T, int G, int mask_mode, int32_t* tiles) {
+  const void* fn = T == 1 ? k1_f32_kernel_g<1>(G, mask_mode)
+                 : T == 2 ? k1_f32_kernel_g<2>(G, mask_mode)
+                 : T == 4 ? k1_f32_kernel_g<4>(G, mask_mode)
+                 : T == 8 ? k1_f32_kernel_g<8>(G, mask_mode)
+                 : T == 16 ? k1_f32_kernel_g<16>(G, mask_mode)
+                 : T == 32 ? k1_f32_kernel_g<32>(G, mask_mode) : nullptr;
+  if (!fn) return hipErrorInvalidValue;
+  int per_cu = 0, dev = 0, cus = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, G * 64, 0);
+  if (e != hipSuccess) return e;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const int M = 3 * per_cu * G * cus / static_cast<int>(2 * kXcds);
+  *tiles = M > 0 ? M : 1;
+  return hipSuccess;
+}
+
 hipError_t launch_k3(const SearchArgs& a, hipStream_t stream) {
   if (a.weights == kWeightsF16) return launch_search_st_f16(a, stream);
   if (a.K != 4) return hipErrorInvalidValue;

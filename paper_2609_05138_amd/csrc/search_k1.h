@@ -340,6 +340,26 @@ k_search(SearchArgs a) {
   }
   const int32_t u0 = a.tile_offset[t];
   const int32_t cnt = a.tile_count[t];
+  // Rotated sweep: the tile's union is swept from entry e0 on, wrapping round,
+  // so that the tiles an XCD runs at once sweep the same part of the feature
+  // range together.  e0 is the tile's phase (as in kernel 3): the plan's
+  // nonzeros of the XCD's earlier tiles, a proxy for their work, over
+  // a.phase_wgs tiles' mean work, mod 1, times the union's size; it depends on
+  // the plan and the tile grid only, not on the slice.
+  int32_t e0 = 0;
+  if (a.rotate && a.chunk_slices <= 1 && cnt > 1) {
+    const int64_t per_xcd = gridDim.x / kXcds;  // tile groups per XCD
+    const int64_t g0 = (blockIdx.x % kXcds) * per_xcd;
+    const int64_t first = a.tile_base + g0 * G;
+    const int64_t end = a.tile_base + (g0 + per_xcd) * G < a.tile_end ? a.tile_base + (g0 + per_xcd) * G : a.tile_end;
+    const uint64_t o_first = static_cast<uint32_t>(a.tile_offset[first]);
+    const uint64_t work = static_cast<uint32_t>(a.tile_offset[end]) - o_first;   // >= cnt > 0
+    const uint64_t nx = static_cast<uint64_t>(end - first);
+    const uint64_t den = static_cast<uint64_t>(a.phase_wgs) * work;
+    const uint64_t num = (static_cast<uint32_t>(u0) - o_first) * nx % den;
+    const uint64_t ph = (num << 20) / den;
+    e0 = __builtin_amdgcn_readfirstlane(static_cast<int32_t>((ph * static_cast<uint64_t>(cnt)) >> 20));
+  }
   const WT* __restrict__ Wn = static_cast<const WT*>(a.W) + n0;
   const int64_t ldw = a.ldw;
 
@@ -370,7 +390,8 @@ k_search(SearchArgs a) {
     // one wave reads and writes its own window: program order suffices
     for (int i = lane; i < kEntryChunk; i += 64) {
       const int32_t idx = base + i;
-      ent[i] = idx < cnt ? make_int2(a.union_feat[u0 + idx], static_cast<int>(a.union_mask[u0 + idx]))
+      const int32_t src = idx + e0 < cnt ? idx + e0 : idx + e0 - cnt;   // rotated sweep (e0 = 0: ascending)
+      ent[i] = idx < cnt ? make_int2(a.union_feat[u0 + src], static_cast<int>(a.union_mask[u0 + src]))
                          : make_int2(0, 0);
     }
     const int32_t rem = cnt - base;
@@ -407,10 +428,15 @@ hipError_t launch_tkg(const SearchArgs& a, hipStream_t stream) {
   // tile groups rounded up to a multiple of the XCD count (see k_search)
   const int64_t groups = (a.tile_end - a.tile_base + G - 1) / G;
   const dim3 grid(static_cast<uint32_t>((groups + kXcds - 1) / kXcds * kXcds), static_cast<uint32_t>(a.nchunks));
+  SearchArgs b = a;
+  if (a.rotate) {
+    const hipError_t e = k1_phase_tiles(T, G, a.mask_mode, &b.phase_wgs);
+    if (e != hipSuccess) return e;
+  }
   if (a.mask_mode == kMaskBranch)
-    hipLaunchKernelGGL((k_search<WT, T, K, G, U, kMaskBranch>), grid, dim3(G * 64), 0, stream, a);
+    hipLaunchKernelGGL((k_search<WT, T, K, G, U, kMaskBranch>), grid, dim3(G * 64), 0, stream, b);
   else
-    hipLaunchKernelGGL((k_search<WT, T, K, G, U, kMaskFma>), grid, dim3(G * 64), 0, stream, a);
+    hipLaunchKernelGGL((k_search<WT, T, K, G, U, kMaskFma>), grid, dim3(G * 64), 0, stream, b);
   return hipGetLastError();
 }
 

@@ -173,22 +173,23 @@ def test_search_rejects_bad_arguments(lib):
                 O(1, 0, 0, 0, 0, 0, 0, 0, 0, 100), O(3, 0, 0, 0, 0, 0, 0, 0, 0, -256),
                 O(2, 0, 0, 0, 0, 0, 0, 0, 0, 256), O(3, 0, 0, 0, 0, 0, 0, 0, 2, 256),
                 O(1, 0, 8, 0, 0, 0, 0, 0, 0, 256),
-                # sweep: 0, 1 or 2; the rotated sweep needs kernel 3's document-major single
-                # launch of one-slice chunks
+                # sweep: 0, 1 or 2; the rotated sweep needs kernel 1 or kernel 3's
+                # document-major form as one launch of one-slice chunks
                 O(0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 3), O(3, 0, 0, 0, 0, 0, 0, 0, 0, 0, -1),
-                O(1, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2), O(2, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2),
-                O(3, 0, 0, 0, 1, 0, 0, 0, 0, 0, 2), O(3, 0, 0, 0, 0, 0, 0, 0, 2, 0, 2),
-                O(0, 16, 0, 0, 0, 0, 0, 0, 0, 0, 2)):
+                O(2, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2),
+                O(3, 0, 0, 0, 1, 0, 0, 0, 0, 0, 2), O(3, 0, 0, 0, 0, 0, 0, 0, 2, 0, 2)):
         st, msg = call(opts=ctypes.byref(bad))
         assert st == som.SOM_ERR_INVALID_ARG, msg
     # rotated sweeps with chunks of two slices (the map has four)
-    st, msg = call(opts=ctypes.byref(O(3, 0, 0, 0, 0, 0, 0, 0, 0, 512, 2)), N=1024, ldw=1024)
-    assert st == som.SOM_ERR_INVALID_ARG and "sweep" in msg, msg
+    for k in (1, 3):
+        st, msg = call(opts=ctypes.byref(O(k, 0, 4, 0, 0, 0, 0, 0, 0, 512, 2)), N=1024, ldw=1024)
+        assert st == som.SOM_ERR_INVALID_ARG and "sweep" in msg, (k, msg)
     # a chunk wider than the map covers it whole
     assert call(opts=ctypes.byref(O(1, 0, 0, 0, 0, 0, 0, 0, 0, 1 << 20)), ws=fake, B=0, nnz=0, indices=null,
                 bmu=null, dist=null)[0] == som.SOM_OK
     # the rotated sweep with one-slice chunks, the ascending sweep anywhere
     for good in (O(0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2), O(3, 128, 0, 0, 2, 0, 0, 0, 1, 256, 2),
+                 O(1, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2), O(1, 4, 0, 2, 1, 0, 0, 0, 0, 256, 2),
                  O(2, 0, 0, 0, 0, 0, 0, 0, 0, 0, 1), O(3, 0, 0, 0, 1, 0, 0, 0, 2, 0, 1)):
         assert call(opts=ctypes.byref(good), ws=fake, B=0, nnz=0, indices=null, bmu=null,
                     dist=null)[0] == som.SOM_OK
@@ -284,7 +285,8 @@ def test_unfused_rejects_bad_arguments(lib):
         return _status(lib, "som_bmu_search_unfused", fake, 8, 8, 8, fake, fake, fake, 4, 10, null, fake, fake,
                        ctypes.byref(o), block, fake, ws_bytes, null)
 
-    for bad in (dict(opts=O(2)), dict(opts=O(3)), dict(block=0), dict(block=12), dict(block=-8)):
+    for bad in (dict(opts=O(2)), dict(opts=O(3)), dict(block=0), dict(block=12), dict(block=-8),
+                dict(opts=O(1, 0, 0, 0, 0, 0, 0, 0, 0, 0, 2))):   # the comparator sweeps in ascending order
         st, msg = call(**bad)
         assert st == som.SOM_ERR_INVALID_ARG, (bad, msg)
     assert call(ws_bytes=64)[0] == som.SOM_ERR_WORKSPACE

@@ -143,7 +143,7 @@ def test_config2_every_document_of_the_first_batch():
     indptr, indices, ip, ix = P.batch(0)
     perm = som.som_cluster_order(ip, ix, P.cfg.F)
     bmu, dist = P.search(ip, ix, perm)
-    b1, d1 = P.search(ip, ix, perm, kernel=1)
+    b1, d1 = P.search(ip, ix, perm, kernel=1, sweep=1)
     b3, d3 = P.search(ip, ix, perm, sweep=1)
     assert torch.equal(b1, b3) and torch.equal(d1, d3), "kernel 1 differs from kernel 3"
     bmu, dist = _host(bmu, dist)
@@ -164,7 +164,7 @@ def test_config3_sample_over_every_batch():
         indptr, indices, ip, ix = P.batch(b)
         bmu, dist = P.search(ip, ix, None)
         if b == nb - 1:   # ascending sweeps of kernels 1 and 3: the same bits on a whole batch
-            b1, d1 = P.search(ip, ix, None, kernel=1)
+            b1, d1 = P.search(ip, ix, None, kernel=1, sweep=1)
             b3, d3 = P.search(ip, ix, None, sweep=1)
             assert torch.equal(b3, b1) and torch.equal(d3, d1), "kernel 1 differs from kernel 3"
             del b1, d1, b3, d3
@@ -184,7 +184,8 @@ def test_config4_sample_over_both_batches():
     # kernel 3 and kernel 1 (16-document tiles, four and one per workgroup)
     # for identical bits, the top-2 search (same first place, second place
     # against the oracle) and the fp16 codebook (automatic: kernel 1,
-    # 8-document tiles; kernel 3 with the ascending sweep for identical bits).
+    # 8-document tiles, rotated sweep, against the oracle; kernels 1 and 3 with
+    # the ascending sweep for identical bits).
     P = _Pass(4)
     bad = []
     for b in (0, 1):
@@ -196,9 +197,9 @@ def test_config4_sample_over_both_batches():
         half = None
         if b == 0:
             ba, da = P.search(ip, ix, perm, sweep=1)
-            b1, d1 = P.search(ip, ix, perm, group_tiles=1)
+            b1, d1 = P.search(ip, ix, perm, group_tiles=1, sweep=1)
             assert torch.equal(b1, ba) and torch.equal(d1, da), "kernel 1, one tile per workgroup, differs"
-            b3, d3 = P.search(ip, ix, perm, kernel=1)
+            b3, d3 = P.search(ip, ix, perm, kernel=1, sweep=1)
             assert torch.equal(b3, ba) and torch.equal(d3, da), "kernel 1 differs from kernel 3"
             flips = int((ba != bmu).sum().item())
             assert flips <= 50 and not torch.equal(da, dist), flips   # rounding only; the rotation is in effect
@@ -210,9 +211,10 @@ def test_config4_sample_over_both_batches():
             W16d = P.Wd.half()
             n16 = som.som_codebook_norms(W16d, N=P.cfg.N)
             half = _host(*som.som_bmu_search(W16d, n16, ip, ix, N=P.cfg.N, perm=perm))
+            h1 = _host(*som.som_bmu_search(W16d, n16, ip, ix, N=P.cfg.N, perm=perm, sweep=1))
             h3 = _host(*som.som_bmu_search(W16d, n16, ip, ix, N=P.cfg.N, perm=perm, kernel=3, sweep=1))
-            assert np.array_equal(h3[0], half[0]) and np.array_equal(h3[1], half[1]), "fp16 kernel 3 differs"
-            del W16d, n16, h3
+            assert np.array_equal(h3[0], h1[0]) and np.array_equal(h3[1], h1[1]), "fp16 kernel 3 differs"
+            del W16d, n16, h1, h3
             torch.cuda.empty_cache()
         bmu, dist = _host(bmu, dist)
         _distance_property(P.W, P.norms64, indptr, indices, bmu.astype(np.int64), dist.astype(np.float64))
@@ -242,7 +244,7 @@ def test_config5_first_middle_and_last_batches():
         perm = som.som_cluster_order(ip, ix, P.cfg.F)
         bmu, dist = P.search(ip, ix, perm)
         if b == 26:
-            b1, d1 = P.search(ip, ix, perm, kernel=1)
+            b1, d1 = P.search(ip, ix, perm, kernel=1, sweep=1)
             b3, d3 = P.search(ip, ix, perm, sweep=1)
             assert torch.equal(b1, b3) and torch.equal(d1, d3), "kernel 1 differs from kernel 3"
             del b1, d1, b3, d3

@@ -139,8 +139,9 @@ def test_f16_equals_fp32_search_of_the_widened_codebook():
                        **{**knobs, "sweep": 1})
             for a, b in zip(out, ref):
                 assert np.array_equal(a, b), knobs
-    # kernel 3's rotated sweep takes the same order for both storage types
-    for knobs in (dict(kernel=3), dict(kernel=3, tile_docs=128)):
+    # the rotated sweeps take the same order for both storage types
+    for knobs in (dict(kernel=3), dict(kernel=3, tile_docs=128), dict(kernel=1, tile_docs=8, lane_neurons=8),
+                  dict(kernel=1, tile_docs=4, lane_neurons=8, group_tiles=2)):
         for p in (None, perm):
             r32 = _run(W16, indptr, indices, top2=True, perm=p, dtype=np.float32, ldw=som.som_codebook_ldw(4100),
                        **knobs)

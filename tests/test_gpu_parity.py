@@ -277,7 +277,7 @@ def test_config2_first_batch():
     bmu, dist, _ = _search(W, indptr, indices, ldw=ldw, perm=perm)
     # ascending sweeps: kernel 3 on the clustered order and kernel 1 on the
     # input order give the same bits on the whole batch
-    b1, d1, _ = _search(W, indptr, indices, ldw=ldw, kernel=1)
+    b1, d1, _ = _search(W, indptr, indices, ldw=ldw, kernel=1, sweep=1)
     b3, d3, _ = _search(W, indptr, indices, ldw=ldw, perm=perm, kernel=3, sweep=1)
     assert np.array_equal(b3, b1) and np.array_equal(d3, d1)
     # the rotated sweep sums in another order: some distances differ in
@@ -327,13 +327,13 @@ def test_results_identical_across_tile_chunk_and_order():
                  dict(kernel=3, neuron_chunk=256, sweep=1), dict(kernel=3, schedule=2)]
     for i, v in enumerate(variants):
         for perm in perms if (i % 5 == 0 or v["kernel"] == 3) else perms[:2]:
-            out = _search(W, indptr, indices, perm=perm, **v)
+            out = _search(W, indptr, indices, perm=perm, **{**v, "sweep": 1})
             if ref is None:
                 ref = out
             assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), v
     # the row stride is a layout choice only
     for ldw in (som.som_codebook_ldw(4100), 4104, 4100 + 1024):
-        for v in (dict(sweep=1), dict(kernel=1, lane_neurons=8), dict(kernel=2), dict(kernel=3, sweep=1)):
+        for v in (dict(sweep=1), dict(kernel=1, lane_neurons=8, sweep=1), dict(kernel=2), dict(kernel=3, sweep=1)):
             out = _search(W, indptr, indices, ldw=ldw, **v)
             assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (ldw, v)
 
@@ -349,7 +349,7 @@ def test_repeated_runs_are_bit_identical():
 
 
 def test_rotated_sweep_order_is_fixed_and_within_tolerance():
-    """Kernel 3's rotated sweep (its automatic order): the order depends on the
+    """Rotated sweeps (the automatic order of kernels 3 and 1): the order depends on the
     plan and the launch's tile grid only, so the results are the same across
     repeated calls, row strides, planned and unplanned searches, top-2 and
     one-slice schedule chunks; they differ from the ascending sweep's only in
@@ -384,6 +384,29 @@ def test_rotated_sweep_order_is_fixed_and_within_tolerance():
         assert rel.max() <= 1e-6, (D, rel.max())
         _check_docs(W64, norms64, indptr, indices, ref[0], ref[1], range(3000))
         del Wd, norms, plan
+    # kernel 1's rotated sweep (its automatic order): the same properties
+    for k1 in (dict(kernel=1), dict(kernel=1, tile_docs=16, group_tiles=4), dict(kernel=1, tile_docs=2, mask_mode=1)):
+        ref = _search(W, indptr, indices, perm=perm, **k1)
+        for v in (dict(sweep=2), dict(neuron_chunk=256)):
+            out = _search(W, indptr, indices, perm=perm, **k1, **v)
+            assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), (k1, v)
+        out = _search(W, indptr, indices, perm=perm, ldw=4100 + 1024, **k1)
+        assert np.array_equal(out[0], ref[0]) and np.array_equal(out[1], ref[1]), k1
+        Wd, _ = _dev_W(W)
+        norms = som.som_codebook_norms(Wd, N=4100)
+        ip, ix, pd = _dev_i32(indptr), _dev_i32(indices), _dev_i32(perm)
+        plan = som.som_plan(ip, ix, 20000, perm=pd, **k1)
+        pl = som.som_bmu_search_planned(Wd, norms, ip, plan, N=4100)
+        t2 = som.som_bmu_search_top2(Wd, norms, ip, ix, N=4100, perm=pd, **k1)
+        torch.cuda.synchronize()
+        for b, d in (pl, t2[:2]):
+            assert np.array_equal(b.cpu().numpy(), ref[0]) and np.array_equal(d.cpu().numpy(), ref[1]), k1
+        asc = _search(W, indptr, indices, perm=perm, sweep=1, **k1)
+        assert not np.array_equal(asc[1], ref[1]), k1
+        rel = np.abs(asc[1].astype(np.float64) - ref[1]) / np.abs(asc[1].astype(np.float64))
+        assert rel.max() <= 1e-6, (k1, rel.max())
+        _check_docs(W64, norms64, indptr, indices, ref[0], ref[1], range(0, 3000, 3))
+        del Wd, norms, plan
 
 
 def test_rotated_sweep_exact_on_a_dyadic_codebook():
@@ -406,7 +429,8 @@ def test_rotated_sweep_exact_on_a_dyadic_codebook():
     want_d = [Fraction(e[1], 16) for e in exact]
     perm = oracle.cluster_order(indptr, indices, F)
     for knobs in (dict(), dict(sweep=2), dict(tile_docs=128), dict(sweep=2, neuron_chunk=256),
-                  dict(sweep=1), dict(kernel=1)):
+                  dict(sweep=1), dict(kernel=1), dict(kernel=1, tile_docs=16, group_tiles=4, sweep=2),
+                  dict(kernel=1, tile_docs=4, mask_mode=1), dict(kernel=1, sweep=1)):
         for p in (None, perm):
             bmu, dist, _ = _search(W, indptr, indices, perm=p, **knobs)
             assert bmu.tolist() == want_b, knobs
@@ -465,12 +489,12 @@ def test_largest_neuron_count_of_one_launch():
     ip, ix = _dev_i32(indptr), _dev_i32(indices)
     first = None
     for knobs in (dict(), dict(kernel=1, tile_docs=16), dict(kernel=1, lane_neurons=8), dict(kernel=3)):
-        bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=NMAX, **knobs)
+        bmu, dist = som.som_bmu_search(Wd, norms, ip, ix, N=NMAX, sweep=1, **knobs)
         torch.cuda.synchronize()
         b, dd = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
         assert (b[1], b[2], b[3]) == (NMAX - 1, NMAX - 300, 5), (knobs, b[1:4])
         assert np.all(dd[1:4] == 0.0)
-        if first is None:   # the oracle once; every launch form sums in the same order
+        if first is None:   # the oracle once; with the ascending sweep every launch form sums in the same order
             _check_docs(W64, norms64, indptr, indices, b, dd, range(len(docs)), N=NMAX)
             first = (b, dd)
         else:
@@ -512,7 +536,7 @@ def test_largest_tile_count_of_one_launch():
     ipB = _dev_i32(indptr[:B + 1])
     nnzB = int(indptr[B])
     ixB = _dev_i32(indices[:nnzB])
-    bmu, dist = som.som_bmu_search(Wd, norms, ipB, ixB, N=N, tile_docs=1)
+    bmu, dist = som.som_bmu_search(Wd, norms, ipB, ixB, N=N, tile_docs=1, sweep=1)
     torch.cuda.synchronize()
     b, dd = bmu.cpu().numpy().astype(np.int64), dist.cpu().numpy().astype(np.float64)
     empty = lens[:B] == 0
@@ -524,7 +548,7 @@ def test_largest_tile_count_of_one_launch():
     with pytest.raises(som.SomError) as e:
         som.som_bmu_search(Wd, norms, ip1, ix1, N=N, tile_docs=1)
     assert e.value.status == 1 and "too many tiles" in str(e.value)
-    bmu2, dist2 = som.som_bmu_search(Wd, norms, ip1, ix1, N=N, tile_docs=2)
+    bmu2, dist2 = som.som_bmu_search(Wd, norms, ip1, ix1, N=N, tile_docs=2, sweep=1)
     torch.cuda.synchronize()
     b2, d2 = bmu2.cpu().numpy().astype(np.int64), dist2.cpu().numpy().astype(np.float64)
     assert np.array_equal(b2[:B], b) and np.array_equal(d2[:B], dd)
@@ -641,14 +665,14 @@ def test_planned_search_reuses_a_plan_across_codebooks():
     ip, ix = _dev_i32(indptr), _dev_i32(indices)
     perm = _dev_i32(oracle.cluster_order(indptr, indices, 2048))
     plan = som.som_plan(ip, ix, 2048, perm=perm, sweep=1)       # kernel 3, ascending sweep
-    plan1 = som.som_plan(ip, ix, 2048, perm=perm, kernel=1, tile_docs=4)
+    plan1 = som.som_plan(ip, ix, 2048, perm=perm, kernel=1, tile_docs=4, sweep=1)
     planr = som.som_plan(ip, ix, 2048, perm=perm)                # kernel 3, rotated sweep
     for seed in (0, 1):
         W = codebook(1, seed=seed)
         Wd, _ = _dev_W(W)
         norms = som.som_codebook_norms(Wd)
         a = som.som_bmu_search_planned(Wd, norms, ip, plan)
-        b = som.som_bmu_search(Wd, norms, ip, ix, perm=perm, kernel=1, tile_docs=4)
+        b = som.som_bmu_search(Wd, norms, ip, ix, perm=perm, kernel=1, tile_docs=4, sweep=1)
         c = som.som_bmu_search_planned(Wd, norms, ip, plan1)
         r = som.som_bmu_search_planned(Wd, norms, ip, planr)
         r0 = som.som_bmu_search(Wd, norms, ip, ix, perm=perm)

@@ -150,10 +150,11 @@ def test_top2_agrees_with_plain_search_and_across_knobs():
             if ref is None:
                 ref = out
             assert np.array_equal(out[2], ref[2]) and np.array_equal(out[3], ref[3]), knobs
-    # the rotated sweep (kernel 3's automatic order): the first place equals
+    # the rotated sweeps (the automatic order of kernels 3 and 1): the first place equals
     # the plain search's with the same plan, the pair is accepted by the oracle
     rot = {}
-    for knobs in (dict(), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256)):
+    for knobs in (dict(), dict(kernel=3, tile_docs=128), dict(kernel=3, tile_docs=256), dict(kernel=1),
+                  dict(kernel=1, tile_docs=4, group_tiles=4)):
         for p in perms:
             pd = None if p is None else _i32(p)
             out = [t.cpu().numpy() for t in som.som_bmu_search_top2(Wd, norms, ip, ix, N=4100, perm=pd, **knobs)]
