@@ -44,7 +44,10 @@ if ROOT not in sys.path:
 L2_PEAK_BPS = 8 * 16 * 128 * 2.4e9
 HBM_PEAK_BPS = 8.0e12
 VALU_PEAK_ADDS = 256 * 128 * 2.4e9       # 256 CUs x 128 fp32 lanes/clk x 2.4 GHz
-LDS_PEAK_BPS = 256 * 128 * 2.4e9         # 256 CUs x 128 B/clk x 2.4 GHz (derived)
+# LDS: one 64-lane 128-bit read (1 KB) per 4 clocks and CU, the rate at which
+# the LDS index-active counter charges such reads (derived; the in-run LDS
+# probe measures what a read loop sustains)
+LDS_PEAK_BPS = 256 * 256 * 2.4e9         # 256 CUs x 256 B/clk x 2.4 GHz
 REL = 1e-5
 
 # Fabric (memory-side cache + HBM) bytes read and written per search launch,
@@ -58,8 +61,8 @@ MEASURED_TRAFFIC = {
     json.dumps(["map512x512-F20000-2M", [0, 1], 0, 262208, "f32", False, False, False, False,
                 {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
                  "schedule": 0, "slice_neurons": 0, "storage": 0, "sweep": 0, "tile_docs": 0}]): {
-        "csrc": "6892385d1fb5cec3",
-        "fetch_kib": [5.3862e9, 4.8464e9],       # per search launch (batch 0, batch 1)
+        "csrc": "472a5147c0f0a07f",
+        "fetch_kib": [5.3876e9, 4.8234e9],       # per search launch (batch 0, batch 1)
         "write_kib": [3.3554e7, 3.0446e7],
         "fetch_scale": 2.0, "write_scale": 1.0,   # plain 4 GiB device copy: FETCH_SIZE reads half, WRITE_SIZE exact
         "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,2>, "
@@ -69,8 +72,8 @@ MEASURED_TRAFFIC = {
     json.dumps(["map512x512-F20000-26.9M-topics", [0], 0, 262208, "f32", False, False, False, False,
                 {"group_tiles": 0, "kernel": 0, "lane_neurons": 0, "mask_mode": 0, "neuron_chunk": 0,
                  "schedule": 0, "slice_neurons": 0, "storage": 0, "sweep": 0, "tile_docs": 0}]): {
-        "csrc": "6892385d1fb5cec3",
-        "fetch_kib": [1.3539e10],
+        "csrc": "472a5147c0f0a07f",
+        "fetch_kib": [1.3540e10],
         "write_kib": [3.2000e7],
         "fetch_scale": 2.0, "write_scale": 1.0,
         "source": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, k_search_st<float,8,4,8,16,2,2>, "
@@ -543,9 +546,19 @@ def main():
             torch.cuda.synchronize()
             return nbytes * passes / (e0.elapsed_time(e1) * 1e-3)
 
+        def lds_rate(iters):
+            som.som_probe_lds(iters, sink)
+            e0, e1 = ev(), ev()
+            e0.record(stream)
+            nbytes = som.som_probe_lds(iters, sink)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return nbytes / (e0.elapsed_time(e1) * 1e-3)
+
         probes = {"l2_GBps": max(max(rate(16 << 20, 200), rate(32 << 20, 100)) for _ in range(3)) / 1e9,
                   "mall_GBps": max(rate(192 << 20, 20) for _ in range(3)) / 1e9,
-                  "hbm_GBps": rate(wbytes_all // 16 * 16, 1) / 1e9}
+                  "hbm_GBps": rate(wbytes_all // 16 * 16, 1) / 1e9,
+                  "lds_GBps": max(lds_rate(1 << 15) for _ in range(3)) / 1e9}
         log(args, "probes: " + ", ".join(f"{k} {v:.0f}" for k, v in probes.items()))
 
     # ---- algorithmic bytes of every search launch (from the plan's per-tile union sizes) ----
@@ -656,6 +669,8 @@ def main():
         # (direct-to-LDS loads) and reads it from LDS once per membership
         lds_bytes = (float(sum(nnzs)) + float(union_total)) * N * wbytes
         levels["lds_algorithmic_vs_derived_lds_peak"] = lds_bytes / float(np.sum(search_s)) / LDS_PEAK_BPS
+        if probes:
+            levels["lds_algorithmic_vs_measured_lds"] = lds_bytes / float(np.sum(search_s)) / (probes["lds_GBps"] * 1e9)
     if traffic is not None:
         fab = traffic * len(batches) / float(np.sum(search_s))
         levels["fabric_measured_vs_hbm_peak"] = fab / HBM_PEAK_BPS

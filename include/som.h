@@ -444,6 +444,18 @@ som_status som_update_finish_f16(uint16_t* W, int64_t F, int64_t ldw, int32_t ro
  * ------------------------------------------------------------------------- */
 som_status som_probe_read(const void* buf, int64_t bytes, int32_t passes, uint32_t* sink, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Measurement aid: LDS read probe.  Launches four 512-thread workgroups per
+ * CU (the residency of the shared-union search kernel), each holding a 32 KB
+ * LDS buffer; every wave reads `iters` 1 KB rows of it (64 lanes x 128 bits,
+ * another row each read) and folds each into four adds.  `iters`: a multiple
+ * of 4 in [4, 2^24].  `sink` (4 bytes of device memory) is written only for
+ * one value of the folded data.  On success `*bytes` (host memory) holds the
+ * bytes the launch reads from LDS: time the call with events on `stream`,
+ * *bytes / time is the LDS read rate.  Nothing is allocated.
+ * ------------------------------------------------------------------------- */
+som_status som_probe_lds(int32_t iters, uint32_t* sink, int64_t* bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

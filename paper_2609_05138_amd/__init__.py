@@ -27,6 +27,7 @@ from .som import (  # noqa: F401
     som_codebook_norms,
     som_last_error,
     som_probe_read,
+    som_probe_lds,
     som_tile_plan,
     som_update_accumulate,
     som_update_finish,

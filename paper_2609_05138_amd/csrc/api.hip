@@ -915,4 +915,14 @@ som_status som_probe_read(const void* buf, int64_t bytes, int32_t passes, uint32
   return ok();
 }
 
+som_status som_probe_lds(int32_t iters, uint32_t* sink, int64_t* bytes, hipStream_t stream) {
+  if (!sink || !bytes) return fail(SOM_ERR_INVALID_ARG, "sink or bytes is NULL");
+  if (!aligned(sink, 4)) return fail(SOM_ERR_INVALID_ARG, "sink must be 4-byte aligned");
+  if (iters < 4 || iters % 4 != 0 || iters > (1 << 24))
+    return fail(SOM_ERR_INVALID_ARG, "iters must be a multiple of 4 in [4, 2^24]");
+  hipError_t e = som::launch_lds_probe(iters, sink, bytes, stream);
+  if (e != hipSuccess) return hip_fail(e, "LDS probe launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -170,6 +170,7 @@ hipError_t launch_update_finish(void* W, int weights, int64_t F, int64_t ldw, in
 
 // Read-bandwidth probe (probe.hip): `passes` grid-stride reads of buf.
 hipError_t launch_read_probe(const void* buf, int64_t bytes, int32_t passes, uint32_t* sink, hipStream_t stream);
+hipError_t launch_lds_probe(int32_t iters, uint32_t* sink, int64_t* bytes, hipStream_t stream);
 
 // Clustering: df histogram, signatures and a bitonic sort of n2 =
 // cluster_sort_size(B) (a power of two >= B) (key, position) pairs.

@@ -13,6 +13,12 @@
 // re-reads.  With a buffer larger than the L2s but smaller than the
 // memory-side cache, the passes after the first measure that cache; a buffer
 // of many GB read once measures HBM.
+//
+// LDS read probe: the roof of the shared-union kernel's row reads.  Every
+// wave of four 8-wave workgroups per CU (the residency of that kernel) reads
+// whole 1 KB rows of a 32 KB LDS buffer with 128-bit loads, the row moving
+// every read, and folds them into registers with four adds per read (as the
+// kernel adds a row into a document's accumulators).
 #include "common.h"
 
 namespace som {
@@ -60,7 +66,48 @@ k_read_probe(const uint4* __restrict__ buf, int64_t n16, int32_t passes, uint32_
   if (x == 0x9e3779b9u) sink[0] = x;
 }
 
+constexpr int kLdsThreads = 512;   // 8 waves
+constexpr int kLdsRows = 32;       // 1 KB rows: a 32 KB buffer
+constexpr int kLdsWgsPerCu = 4;
+
+__global__ void __launch_bounds__(kLdsThreads)
+k_lds_probe(int32_t iters, uint32_t* __restrict__ sink) {
+  __shared__ uint4 rows[kLdsRows * 64];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  for (int i = t; i < kLdsRows * 64; i += kLdsThreads)
+    rows[i] = make_uint4(static_cast<uint32_t>(i), 3u * i, 5u * i, 7u * i);
+  __syncthreads();
+  uint32_t x[4][4] = {};
+  for (int32_t i = 0; i < iters; i += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      // row (5 (i + u) + 3 w) mod 32: another row for every read and wave
+      const uint4 v = rows[(((i + u) * 5 + w * 3) & (kLdsRows - 1)) * 64 + lane];
+      x[u][0] += v.x;
+      x[u][1] += v.y;
+      x[u][2] += v.z;
+      x[u][3] += v.w;
+    }
+  }
+  uint32_t f = 0u;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) f ^= x[u][0] ^ x[u][1] ^ x[u][2] ^ x[u][3];
+  if (f == 0x9e3779b9u) sink[0] = f;
+}
+
 }  // namespace
+
+hipError_t launch_lds_probe(int32_t iters, uint32_t* sink, int64_t* bytes, hipStream_t stream) {
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const int64_t wgs = static_cast<int64_t>(cus > 0 ? cus : 256) * kLdsWgsPerCu;
+  *bytes = wgs * (kLdsThreads / 64) * static_cast<int64_t>(iters) * 1024;
+  hipLaunchKernelGGL(k_lds_probe, dim3(static_cast<uint32_t>(wgs)), dim3(kLdsThreads), 0, stream, iters, sink);
+  return hipGetLastError();
+}
 
 hipError_t launch_read_probe(const void* buf, int64_t bytes, int32_t passes, uint32_t* sink, hipStream_t stream) {
   int dev = 0, cus = 0;

@@ -54,6 +54,7 @@ EXPORTS = (
     "som_update_finish",
     "som_update_finish_f16",
     "som_probe_read",
+    "som_probe_lds",
 )
 
 
@@ -154,6 +155,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         fn.argtypes = [_vp, _i64, _i64, _i32, _i32, ctypes.c_double, _vp, _i64, _vp, _vp, _sz, _vp]
     lib.som_probe_read.restype = _i32
     lib.som_probe_read.argtypes = [_vp, _i64, _i32, _vp, _vp]
+    lib.som_probe_lds.restype = _i32
+    lib.som_probe_lds.argtypes = [_i32, _vp, ctypes.POINTER(ctypes.c_int64), _vp]
     lib.som_cluster_order.restype = _i32
     lib.som_cluster_order.argtypes = [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _sz, _vp]
     _lib = lib
@@ -596,4 +599,13 @@ def som_probe_read(buf: torch.Tensor, nbytes: int, passes: int = 1, sink: Option
     if sink is None:
         sink = torch.empty(1, dtype=torch.int32, device=buf.device)
     _check(lib.som_probe_read(_ptr(buf), int(nbytes), int(passes), _ptr(sink), _stream(stream)))
+
+
+def som_probe_lds(iters: int, sink: torch.Tensor, stream=None) -> int:
+    """LDS read probe (see som.h); returns the bytes the launch reads from LDS."""
+    lib = load()
+    _dev(sink, torch.int32, "sink")
+    nbytes = ctypes.c_int64(0)
+    _check(lib.som_probe_lds(int(iters), _ptr(sink), ctypes.byref(nbytes), _stream(stream)))
+    return int(nbytes.value)
 

@@ -77,6 +77,13 @@ def test_probe_rejects_bad_arguments(lib):
                  (ctypes.c_void_p(0x1004), 64, 1, fake), (fake, 64, 0, fake)):
         st, _ = _status(lib, "som_probe_read", *args, None)
         assert st == som.SOM_ERR_INVALID_ARG, args
+    n = ctypes.c_int64(-1)
+    for args in ((4, None, ctypes.byref(n)), (4, fake, None), (4, ctypes.c_void_p(0x1002), ctypes.byref(n)),
+                 (0, fake, ctypes.byref(n)), (3, fake, ctypes.byref(n)), (6, fake, ctypes.byref(n)),
+                 (-4, fake, ctypes.byref(n)), ((1 << 24) + 4, fake, ctypes.byref(n))):
+        st, _ = _status(lib, "som_probe_lds", *args, None)
+        assert st == som.SOM_ERR_INVALID_ARG, args
+    assert n.value == -1                    # nothing written on a rejected call
 
 
 def test_codebook_ldw_is_host_only(lib):

@@ -696,3 +696,13 @@ def test_read_probe_runs_and_leaves_the_buffer_alone():
         som.som_probe_read(buf, nbytes, passes, sink)
     torch.cuda.synchronize()
     assert torch.equal(buf, ref)
+
+
+def test_lds_probe_reports_its_bytes():
+    """The LDS probe runs four 8-wave workgroups per CU, each wave reading
+    `iters` 1 KB rows, and reports exactly those bytes."""
+    sink = torch.zeros(1, dtype=torch.int32, device=DEV)
+    cus = torch.cuda.get_device_properties(DEV).multi_processor_count
+    for iters in (4, 1024):
+        assert som.som_probe_lds(iters, sink) == cus * 4 * 8 * iters * 1024
+    torch.cuda.synchronize()
